@@ -1,0 +1,191 @@
+/*
+ * inferscale.h -- C ABI of the MI355X (gfx950) retrieve + Chunked-RoPE
+ * KV-inject library (libinferscale.so).
+ *
+ * The serving-time hot path of InferScale, as three calls:
+ *   is_retrieve  exact top-k facts by inner product of a query embedding with
+ *                a GPU-resident embedding bank (§3.2 "Persistent memory store
+ *                and retrieval": the query embedding issues a top-k search
+ *                that yields fact ids);
+ *   is_slot_map  places the retrieved facts contiguously, most relevant fact
+ *                adjacent to the query (§5.2 "Position policy"), and maps
+ *                every placed token to its position and to its slot in a
+ *                paged KV cache through the request's block table (§2.2
+ *                paged blocks; §3.4 the scatter goes through the slot
+ *                mapping);
+ *   is_inject    gathers each placed token's stored pre-RoPE key and value,
+ *                rotates the key to the token's position (§3.3 composition;
+ *                §2.4 and Theorem "Chunked RoPE Injection", §5.1) and writes
+ *                both into the paged cache (§3.4).
+ *
+ * Conventions shared by every call
+ *   - All data pointers are DEVICE pointers owned by the caller. The library
+ *     allocates and frees nothing; retrieval scratch is the caller's
+ *     workspace, sized by is_retrieve_workspace_size.
+ *   - `stream` is a hipStream_t (NULL: the legacy default stream). Every call
+ *     only enqueues work on it and returns; none synchronizes. The calls keep
+ *     no state between invocations and may run concurrently on different
+ *     streams with disjoint outputs.
+ *   - Return value: IS_OK, or a negative IS_ERR_* code for misuse detected on
+ *     the host BEFORE anything is enqueued (null or misaligned pointers, bad
+ *     sizes, unsupported dtype, short workspace), or IS_ERR_HIP when a launch
+ *     fails. is_last_error() returns a message for the calling thread's last
+ *     failure.
+ *   - Errors that depend on device data (an id out of range, a block table
+ *     that is too short, more tokens than max_tokens, ...) are reported by
+ *     OR-ing IS_DEV_* flags into the caller's device word *status (which the
+ *     caller clears). The offending request (slot map) or token/fact (inject)
+ *     is skipped; nothing else about it is written.
+ *   - bf16 is stored as raw 16-bit patterns (the upper half of an IEEE
+ *     binary32).
+ *   - Preconditions the library cannot check cheaply: the destination slots
+ *     of one call are distinct (requests own disjoint blocks), and the page
+ *     pools do not overlap the pre-RoPE store. Violations give unspecified
+ *     page contents but no out-of-bounds access.
+ */
+#ifndef INFERSCALE_H
+#define INFERSCALE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+#define IS_OK 0
+#define IS_ERR_INVALID (-1)      /* bad argument detected on the host        */
+#define IS_ERR_UNSUPPORTED (-2)  /* valid but not supported by this build    */
+#define IS_ERR_WORKSPACE (-3)    /* workspace missing or too small           */
+#define IS_ERR_HIP (-4)          /* the HIP runtime refused a launch         */
+
+/* element types of embeddings */
+#define IS_DTYPE_F32 0
+#define IS_DTYPE_BF16 1
+
+/* device status flags, OR-ed into *status */
+#define IS_DEV_ID_RANGE 1u    /* an id < 0 or >= n                                  */
+#define IS_DEV_BT_SHORT 2u    /* a placed position needs a block index >= max_blocks */
+#define IS_DEV_CAPACITY 4u    /* a request's facts hold more than max_tokens tokens  */
+#define IS_DEV_BAD_LEN 8u     /* a fact length < 0                                  */
+#define IS_DEV_BAD_BLOCK 16u  /* a block-table entry used by a request is < 0        */
+#define IS_DEV_SLOT_RANGE 32u /* a slot outside [0, num_slots)                      */
+#define IS_DEV_SRC_RANGE 64u  /* a fact's stored rows fall outside [0, T_store)      */
+
+/* limits of this build */
+#define IS_MAX_K 1024         /* largest k                                           */
+#define IS_MAX_HEAD_DIM 512   /* largest head dimension D                            */
+
+/* Library version string, e.g. "inferscale-gfx950 0.1.0". */
+const char* is_version(void);
+
+/* Message describing the calling thread's most recent IS_ERR_* return
+ * ("" if none). The pointer stays valid until the thread's next call. */
+const char* is_last_error(void);
+
+/* Bytes of device workspace is_retrieve needs for these sizes (0 on bad
+ * arguments; *bytes receives the size). Arguments as in is_retrieve. */
+int is_retrieve_workspace_size(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dtype,
+                               size_t* bytes);
+
+/*
+ * is_retrieve -- exact top-k by inner product (§3.2).
+ *
+ * For request r < nq with bank B_r = bank + r * bank_stride elements
+ * (bank_stride == 0: every request searches the same bank):
+ *   s_j = sum_t query_emb[r][t] * B_r[j][t],  j < n
+ * accumulated in fp32 (bf16 inputs: exact bf16 x bf16 products, fp32 sums).
+ * Output row r lists the k facts with the highest s_j, best first; equal
+ * scores go to the lower id; -0.0 counts as +0.0 and NaN as the lowest.
+ *
+ *   query_emb  [nq][d] of dtype, 16-byte aligned
+ *   bank       [n][d] (shared) or bank_stride-spaced [n][d] per request,
+ *              row-major, 16-byte aligned, dtype as query_emb
+ *   n          facts per bank, 1 <= n < 2^31
+ *   d          embedding dimension, multiple of 8, 8 <= d <= 8192
+ *   k          1 <= k <= min(n, IS_MAX_K)
+ *   out_ids    [nq][k] int32 device
+ *   out_scores [nq][k] fp32 device (may be NULL)
+ *   nq         number of requests, >= 1
+ *   bank_stride elements between consecutive requests' banks (0 = shared);
+ *              a multiple of 8 elements
+ *   dtype      IS_DTYPE_F32 or IS_DTYPE_BF16
+ *   workspace  device scratch of at least is_retrieve_workspace_size bytes,
+ *              256-byte aligned; its contents are not preserved
+ */
+int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
+                int32_t dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * is_slot_map -- placement and slot mapping (§5.2 Position policy; §2.2).
+ *
+ * For request r with ranked ids[r][0..k-1] (as is_retrieve returns them),
+ * facts C_0..C_{k-1} are placed contiguously: C_i = ids[r][k-1-i] when
+ * reverse_rank != 0 (the most relevant fact last, next to the query), else
+ * C_i = ids[r][i]. With b_0 = 0 and b_{i+1} = b_i + len(C_i), token t of C_i
+ * is placed token b_i + t at position p = start_pos + b_i + t, in slot
+ *   block_table[r][p / page_size] * page_size + p % page_size.
+ * Positions [0, start_pos) belong to the instruction prefix that precedes
+ * the memory (§3.3) and are not touched.
+ *
+ *   ids            [nq][k] int32 device
+ *   fact_lens      per-request [n] int32 tables, lens_stride elements apart
+ *                  (lens_stride 0: one shared table)
+ *   start_pos      first memory position, >= 0
+ *   block_table    [nq][max_blocks] int32 device (physical block ids)
+ *   page_size      tokens per block, >= 1
+ *   out_slots      [nq][max_tokens] int64 device; entries >= m[r] untouched
+ *   out_positions  [nq][max_tokens] int32 device; entries >= m[r] untouched
+ *   out_m          [nq] int32 device: tokens placed (0 for a skipped request)
+ *   k              1 <= k <= IS_MAX_K
+ *   n              facts per table (ids must lie in [0, n))
+ *   max_tokens     capacity per request row, >= 0
+ *   reverse_rank   1: the paper's policy; 0: rank order as given
+ *   status         device uint32 flag word (may be NULL)
+ * A request with an id out of range, a negative length, more than
+ * max_tokens tokens, or positions beyond its block table gets m = 0.
+ */
+int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
+                const int32_t* block_table, int32_t page_size, int64_t* out_slots,
+                int32_t* out_positions, int32_t* out_m, int32_t k, int32_t nq, int64_t n,
+                int64_t lens_stride, int32_t max_blocks, int32_t max_tokens,
+                int32_t reverse_rank, uint32_t* status, void* stream);
+
+/*
+ * is_inject -- fused gather + RoPE + scatter into the paged cache
+ * (§3.3 composition; §3.4 injection; §2.4 / §5.1 rotation).
+ *
+ * For request r, placed token idx < m[r] (fact C_i, in-fact token t, derived
+ * from ids, fact_lens and reverse_rank exactly as in is_slot_map), layer l,
+ * head h:
+ *   src = fact_offsets[r][C_i] + t
+ *   paged_k[l][slots[r][idx]][h][:] = R_p preK[l][src][h][:], p = positions[r][idx]
+ *   paged_v[l][slots[r][idx]][h][:] = V[l][src][h][:]           (bit copy)
+ * R_p rotates pair (j, j + D/2) by the angle p * rope_theta^(-2j/D),
+ * j < D/2. The angle is formed and reduced in fp64, its sine and cosine are
+ * fp32, the rotation is fp32 and each output is rounded to nearest-even bf16.
+ *
+ *   preK, V        bf16 [L][T_store][H][D] device, 16-byte aligned
+ *   slots, positions  [nq][max_tokens] as written by is_slot_map
+ *   paged_k, paged_v  bf16 [L][num_slots][H][D] device, 16-byte aligned
+ *   fact_offsets   per-request [n] int64 row offsets into the store
+ *   fact_lens      per-request [n] int32 (both lens_stride elements apart)
+ *   m              [nq] int32 device, tokens placed per request
+ *   D              head dimension: a multiple of 16, <= IS_MAX_HEAD_DIM
+ * Tokens whose slot lies outside [0, num_slots) and facts whose rows fall
+ * outside the store are skipped and flagged.
+ */
+int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+              const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+              const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+              int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+              int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+              int64_t num_slots, uint32_t* status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INFERSCALE_H */

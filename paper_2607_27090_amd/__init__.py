@@ -1,0 +1,160 @@
+"""Python binding of libinferscale (MI355X / gfx950).
+
+Argument marshalling only: every step of the retrieve + Chunked-RoPE inject
+path runs in the library's HIP kernels. Tensors are torch device tensors;
+their data pointers and torch's current HIP stream are handed to the C ABI
+declared in include/inferscale.h. If the library is not built, importing the
+functions raises: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loaded first so the library binds to torch's HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libinferscale.so")
+
+IS_OK = 0
+IS_ERR_INVALID = -1
+IS_ERR_UNSUPPORTED = -2
+IS_ERR_WORKSPACE = -3
+IS_ERR_HIP = -4
+
+IS_DTYPE_F32 = 0
+IS_DTYPE_BF16 = 1
+
+IS_DEV_ID_RANGE = 1
+IS_DEV_BT_SHORT = 2
+IS_DEV_CAPACITY = 4
+IS_DEV_BAD_LEN = 8
+IS_DEV_BAD_BLOCK = 16
+IS_DEV_SLOT_RANGE = 32
+IS_DEV_SRC_RANGE = 64
+
+IS_MAX_K = 1024
+IS_MAX_HEAD_DIM = 512
+
+EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
+            "is_slot_map", "is_inject")
+
+
+class InferScaleError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn} returned {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libinferscale.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(LIB_PATH, mode=os.RTLD_NOW | os.RTLD_LOCAL)
+    P = ctypes.c_void_p
+    i32, i64, sz, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+    lib.is_version.argtypes = []
+    lib.is_version.restype = ctypes.c_char_p
+    lib.is_last_error.argtypes = []
+    lib.is_last_error.restype = ctypes.c_char_p
+    lib.is_retrieve_workspace_size.argtypes = [i64, i32, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.is_retrieve_workspace_size.restype = ctypes.c_int
+    lib.is_retrieve.argtypes = [P, P, i64, i32, i32, P, P, i32, i64, i32, P, sz, P]
+    lib.is_retrieve.restype = ctypes.c_int
+    lib.is_slot_map.argtypes = [P, P, i32, P, i32, P, P, P, i32, i32, i64, i64, i32, i32, i32, P, P]
+    lib.is_slot_map.restype = ctypes.c_int
+    lib.is_inject.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32, i32,
+                              i32, i32, i32, i64, i64, P, P]
+    lib.is_inject.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != IS_OK:
+        msg = load_library().is_last_error().decode(errors="replace")
+        raise InferScaleError(fn, rc, msg)
+
+
+def _ptr(x):
+    """Device pointer of a tensor (None -> NULL; ints pass through)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not isinstance(x, torch.Tensor):
+        raise TypeError(f"expected a torch tensor, got {type(x)}")
+    if not x.is_cuda:
+        raise ValueError("libinferscale takes device tensors")
+    if not x.is_contiguous():
+        raise ValueError("libinferscale takes contiguous tensors")
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _emb_dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return IS_DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return IS_DTYPE_BF16
+    raise ValueError(f"embeddings must be float32 or bfloat16, got {t.dtype}")
+
+
+def is_version() -> str:
+    return load_library().is_version().decode()
+
+
+def is_retrieve_workspace_size(n: int, d: int, k: int, nq: int = 1,
+                               dtype: int = IS_DTYPE_F32) -> int:
+    out = ctypes.c_size_t(0)
+    _check("is_retrieve_workspace_size",
+           load_library().is_retrieve_workspace_size(n, d, k, nq, dtype, ctypes.byref(out)))
+    return out.value
+
+
+def is_retrieve(query_emb, bank, n, d, k, out_ids, out_scores=None, *, nq=1, bank_stride=0,
+                workspace=None, stream=None) -> None:
+    """Exact top-k by inner product (see include/inferscale.h)."""
+    dt = _emb_dtype(query_emb)
+    if workspace is None:
+        raise ValueError("is_retrieve needs a workspace tensor "
+                         "(is_retrieve_workspace_size bytes of device memory)")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("is_retrieve", load_library().is_retrieve(
+        _ptr(query_emb), _ptr(bank), n, d, k, _ptr(out_ids), _ptr(out_scores), nq, bank_stride,
+        dt, _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def is_slot_map(ids, fact_lens, start_pos, block_table, page_size, out_slots, out_positions,
+                out_m, *, k, nq, n, lens_stride, max_blocks, max_tokens, reverse_rank=1,
+                status=None, stream=None) -> None:
+    """Placement + slot map (see include/inferscale.h)."""
+    _check("is_slot_map", load_library().is_slot_map(
+        _ptr(ids), _ptr(fact_lens), start_pos, _ptr(block_table), page_size, _ptr(out_slots),
+        _ptr(out_positions), _ptr(out_m), k, nq, n, lens_stride, max_blocks, max_tokens,
+        reverse_rank, _ptr(status), _stream(stream)))
+
+
+def is_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *, fact_offsets,
+              fact_lens, m, k, nq, n, lens_stride, reverse_rank=1, max_tokens, L, H, D,
+              T_store, num_slots, status=None, stream=None) -> None:
+    """Fused gather + RoPE + scatter (see include/inferscale.h)."""
+    _check("is_inject", load_library().is_inject(
+        _ptr(ids), _ptr(preK), _ptr(V), _ptr(slots), _ptr(positions), float(rope_theta),
+        _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens), _ptr(m), k, nq, n,
+        lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots, _ptr(status),
+        _stream(stream)))

@@ -1,0 +1,197 @@
+// C ABI of libinferscale: host-side argument validation, workspace layout and
+// launch sequencing. The contract of every entry point is documented in
+// include/inferscale.h.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "launch.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int ok() {
+    g_last_error.clear();
+    return IS_OK;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct RetrieveLayout {
+    size_t scores_off, cand_a_off, cand_b_off, total;
+    int nchunks;
+};
+
+RetrieveLayout retrieve_layout(int64_t n, int32_t k, int32_t nq) {
+    RetrieveLayout lay{};
+    const int64_t chunk = is::select_chunk_len();
+    lay.nchunks = (int)((n + chunk - 1) / chunk);
+    size_t off = 0;
+    lay.scores_off = off;
+    off = round_up(off + (size_t)nq * (size_t)n * sizeof(float), 256);
+    lay.cand_a_off = off;
+    const size_t cand = lay.nchunks > 1 ? (size_t)nq * lay.nchunks * k * sizeof(uint64_t) : 0;
+    off = round_up(off + cand, 256);
+    lay.cand_b_off = off;
+    off = round_up(off + cand, 256);
+    lay.total = off;
+    return lay;
+}
+
+int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dtype) {
+    if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
+    if (d < 8 || d > 8192 || d % 8) return fail(IS_ERR_INVALID, "d=%d must be a multiple of 8 in [8, 8192]", d);
+    if (k < 1 || k > n || k > IS_MAX_K)
+        return fail(IS_ERR_INVALID, "k=%d must be in [1, min(n, %d)]", k, IS_MAX_K);
+    if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
+    if (dtype != IS_DTYPE_F32 && dtype != IS_DTYPE_BF16)
+        return fail(IS_ERR_UNSUPPORTED, "dtype=%d is neither IS_DTYPE_F32 nor IS_DTYPE_BF16", dtype);
+    return IS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* is_version(void) { return "inferscale-gfx950 0.1.0"; }
+
+const char* is_last_error(void) { return g_last_error.c_str(); }
+
+int is_retrieve_workspace_size(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dtype,
+                               size_t* bytes) {
+    if (!bytes) return fail(IS_ERR_INVALID, "bytes is NULL");
+    *bytes = 0;
+    const int rc = check_retrieve_sizes(n, d, k, nq, dtype);
+    if (rc) return rc;
+    *bytes = retrieve_layout(n, k, nq).total;
+    return ok();
+}
+
+int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
+                int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!query_emb || !bank || !out_ids)
+        return fail(IS_ERR_INVALID, "query_emb, bank and out_ids must be non-NULL");
+    int rc = check_retrieve_sizes(n, d, k, nq, dtype);
+    if (rc) return rc;
+    if (bank_stride < 0 || bank_stride % 8)
+        return fail(IS_ERR_INVALID, "bank_stride=%lld must be >= 0 and a multiple of 8",
+                    (long long)bank_stride);
+    if (!aligned(query_emb, 16) || !aligned(bank, 16))
+        return fail(IS_ERR_INVALID, "query_emb and bank must be 16-byte aligned");
+    if (!aligned(out_ids, 4) || (out_scores && !aligned(out_scores, 4)))
+        return fail(IS_ERR_INVALID, "out_ids/out_scores must be 4-byte aligned");
+    const RetrieveLayout lay = retrieve_layout(n, k, nq);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(IS_ERR_INVALID, "workspace must be 256-byte aligned");
+
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    float* scores = (float*)(ws + lay.scores_off);
+    hipError_t e = is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+    if (lay.nchunks == 1) {
+        e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        return ok();
+    }
+    uint64_t* a = (uint64_t*)(ws + lay.cand_a_off);
+    uint64_t* b = (uint64_t*)(ws + lay.cand_b_off);
+    e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, nullptr, nullptr, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+    int64_t M = (int64_t)lay.nchunks * k;
+    const int64_t chunk = is::select_chunk_len();
+    while (M > chunk) {
+        const int nch = (int)((M + chunk - 1) / chunk);
+        e = is::launch_select_keys(a, M, k, nq, nch, b, nullptr, nullptr, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        uint64_t* tmp = a;
+        a = b;
+        b = tmp;
+        M = (int64_t)nch * k;
+    }
+    e = is::launch_select_keys(a, M, k, nq, 1, nullptr, out_ids, out_scores, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
+                const int32_t* block_table, int32_t page_size, int64_t* out_slots,
+                int32_t* out_positions, int32_t* out_m, int32_t k, int32_t nq, int64_t n,
+                int64_t lens_stride, int32_t max_blocks, int32_t max_tokens,
+                int32_t reverse_rank, uint32_t* status, void* stream) {
+    if (!ids || !fact_lens || !block_table || !out_slots || !out_positions || !out_m)
+        return fail(IS_ERR_INVALID, "ids, fact_lens, block_table and outputs must be non-NULL");
+    if (k < 1 || k > IS_MAX_K) return fail(IS_ERR_INVALID, "k=%d must be in [1, %d]", k, IS_MAX_K);
+    if (nq < 1) return fail(IS_ERR_INVALID, "nq=%d must be >= 1", nq);
+    if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
+    if (page_size < 1) return fail(IS_ERR_INVALID, "page_size=%d must be >= 1", page_size);
+    if (start_pos < 0) return fail(IS_ERR_INVALID, "start_pos=%d must be >= 0", start_pos);
+    if (max_blocks < 0 || max_tokens < 0)
+        return fail(IS_ERR_INVALID, "max_blocks and max_tokens must be >= 0");
+    if ((int64_t)start_pos + max_tokens > INT32_MAX)
+        return fail(IS_ERR_INVALID, "start_pos + max_tokens must stay below 2^31");
+    if (lens_stride < 0) return fail(IS_ERR_INVALID, "lens_stride must be >= 0");
+    if (!aligned(out_slots, 8) || !aligned(ids, 4) || !aligned(fact_lens, 4) ||
+        !aligned(block_table, 4) || !aligned(out_positions, 4) || !aligned(out_m, 4) ||
+        (status && !aligned(status, 4)))
+        return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    hipError_t e = is::launch_slot_map(ids, fact_lens, start_pos, block_table, page_size, out_slots,
+                                       out_positions, out_m, k, nq, n, lens_stride, max_blocks,
+                                       max_tokens, reverse_rank, status, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "slot map launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+              const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+              const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+              int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+              int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+              int64_t num_slots, uint32_t* status, void* stream) {
+    if (!ids || !preK || !V || !slots || !positions || !paged_k || !paged_v || !fact_offsets ||
+        !fact_lens || !m)
+        return fail(IS_ERR_INVALID, "every array argument except status must be non-NULL");
+    if (k < 1 || k > IS_MAX_K) return fail(IS_ERR_INVALID, "k=%d must be in [1, %d]", k, IS_MAX_K);
+    if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
+    if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
+    if (L < 1 || H < 1) return fail(IS_ERR_INVALID, "L=%d and H=%d must be >= 1", L, H);
+    if (D < 16 || D % 16 || D > IS_MAX_HEAD_DIM)
+        return fail(IS_ERR_UNSUPPORTED, "D=%d must be a multiple of 16 in [16, %d]", D,
+                    IS_MAX_HEAD_DIM);
+    if ((int64_t)H * D > (1 << 20)) return fail(IS_ERR_UNSUPPORTED, "H*D=%lld too large", (long long)H * D);
+    if (T_store < 0 || num_slots < 0 || max_tokens < 0 || lens_stride < 0)
+        return fail(IS_ERR_INVALID, "T_store, num_slots, max_tokens and lens_stride must be >= 0");
+    if (!(rope_theta > 0.f) || !std::isfinite(rope_theta))
+        return fail(IS_ERR_INVALID, "rope_theta must be positive and finite");
+    if (!aligned(preK, 16) || !aligned(V, 16) || !aligned(paged_k, 16) || !aligned(paged_v, 16))
+        return fail(IS_ERR_INVALID, "preK, V, paged_k and paged_v must be 16-byte aligned");
+    if (!aligned(slots, 8) || !aligned(fact_offsets, 8) || !aligned(ids, 4) ||
+        !aligned(positions, 4) || !aligned(fact_lens, 4) || !aligned(m, 4) ||
+        (status && !aligned(status, 4)))
+        return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    hipError_t e = is::launch_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v,
+                                     fact_offsets, fact_lens, m, k, nq, n, lens_stride,
+                                     reverse_rank, max_tokens, L, H, D, T_store, num_slots, status,
+                                     (hipStream_t)stream);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "inject launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+}  // extern "C"

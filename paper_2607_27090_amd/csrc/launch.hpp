@@ -1,0 +1,38 @@
+// Internal launchers of libinferscale's kernels (host side). The C ABI in
+// abi.hip validates arguments and calls these; each returns the launch
+// status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "inferscale.h"
+
+namespace is {
+
+// retrieve.hip
+hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, int nq,
+                       int64_t bank_stride, int dtype, float* scores, hipStream_t st);
+int64_t select_chunk_len();
+hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
+                                uint64_t* cand, int32_t* out_ids, float* out_scores,
+                                hipStream_t st);
+hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, int nchunks,
+                              uint64_t* cand, int32_t* out_ids, float* out_scores, hipStream_t st);
+
+// place.hip
+hipError_t launch_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
+                           const int32_t* block_table, int32_t page_size, int64_t* out_slots,
+                           int32_t* out_positions, int32_t* out_m, int32_t k, int32_t nq,
+                           int64_t n, int64_t lens_stride, int32_t max_blocks, int32_t max_tokens,
+                           int32_t reverse_rank, uint32_t* status, hipStream_t st);
+
+// inject.hip
+hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+                         const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+                         const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+                         int32_t k, int32_t nq, int64_t n, int64_t lens_stride,
+                         int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
+                         int64_t T_store, int64_t num_slots, uint32_t* status, hipStream_t st);
+
+}  // namespace is

@@ -1,0 +1,357 @@
+// Exact top-k retrieval for gfx950 (§3.2: top-k search by inner product over
+// the fact embeddings; exact brute force stands in for the paper's GPU
+// graph index).
+//
+// Two stages:
+//  1. scan: s_j = <q, e_j> for every bank row. Bandwidth-bound GEMV: each
+//     wave streams whole rows with 16-byte loads, keeps its queries in
+//     registers, and reduces per-row partial sums across the wave with a
+//     transposing butterfly so that V partial sums cost V-1 shuffles.
+//  2. select: radix select of the k largest 64-bit rank keys
+//     (score bits, ~id) per query. One 1024-thread workgroup owns a chunk of
+//     up to 16384 keys in registers; digits are taken 8 bits at a time from
+//     the highest bit in which the chunk's keys differ, until the boundary
+//     digit bucket is taken whole. Chunks emit k candidates each; a final
+//     pass over the candidates orders the winners (score desc, id asc).
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace is {
+
+// ---- scan ------------------------------------------------------------------
+
+struct F32Tag {};
+struct BF16Tag {};
+
+__device__ __forceinline__ float dot16(uint4 a, uint4 b, F32Tag) {
+    float s = __uint_as_float(a.x) * __uint_as_float(b.x);
+    s = fmaf(__uint_as_float(a.y), __uint_as_float(b.y), s);
+    s = fmaf(__uint_as_float(a.z), __uint_as_float(b.z), s);
+    s = fmaf(__uint_as_float(a.w), __uint_as_float(b.w), s);
+    return s;
+}
+
+__device__ __forceinline__ float dot16(uint4 a, uint4 b, BF16Tag) {
+    // bf16 x bf16 products are exact in fp32
+    float s = bf16_lo(a.x) * bf16_lo(b.x);
+    s = fmaf(bf16_hi(a.x), bf16_hi(b.x), s);
+    s = fmaf(bf16_lo(a.y), bf16_lo(b.y), s);
+    s = fmaf(bf16_hi(a.y), bf16_hi(b.y), s);
+    s = fmaf(bf16_lo(a.z), bf16_lo(b.z), s);
+    s = fmaf(bf16_hi(a.z), bf16_hi(b.z), s);
+    s = fmaf(bf16_lo(a.w), bf16_lo(b.w), s);
+    s = fmaf(bf16_hi(a.w), bf16_hi(b.w), s);
+    return s;
+}
+
+// Reduce V partial sums held by every lane of a wave. On return the lane
+// holds the full sum of value index `*which`; lanes whose low (6 - log2 V)
+// bits are zero are the unique holders.
+template <int V>
+__device__ __forceinline__ float wave_multi_sum(float (&a)[V], int lane, int* which) {
+    int idx = 0;
+#pragma unroll
+    for (int half = V / 2, off = 32; half >= 1; half >>= 1, off >>= 1) {
+        const bool upper = (lane & off) != 0;
+#pragma unroll
+        for (int i = 0; i < half; ++i) {
+            float keep = upper ? a[i + half] : a[i];
+            float send = upper ? a[i] : a[i + half];
+            a[i] = keep + __shfl_xor(send, off, kWave);
+        }
+        if (upper) idx += half;
+    }
+    constexpr int kSteps = (V >= 64) ? 0 : 6 - __builtin_ctz(V);
+    float v = a[0];
+#pragma unroll
+    for (int s = 0, off = 32 / V; s < kSteps; ++s, off >>= 1) v += __shfl_xor(v, off, kWave);
+    *which = idx;
+    return v;
+}
+
+// One block = 4 waves. blockIdx.y selects a group of NQB queries (shared
+// bank) or one query and its own bank (per-query banks, NQB == 1).
+template <class Tag, int CPL, int NQB, int RB>
+__global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ query,
+                                                   const uint4* __restrict__ bank, int64_t n,
+                                                   int chunks, int nq, int64_t bank_stride_chunks,
+                                                   int rows_per_block, float* __restrict__ scores) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int q0 = blockIdx.y * NQB;
+    const uint4* B = bank + (int64_t)blockIdx.y * bank_stride_chunks;
+
+    uint4 qr[NQB][CPL];
+#pragma unroll
+    for (int qq = 0; qq < NQB; ++qq)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int ci = lane + c * kWave;
+            qr[qq][c] = (q0 + qq < nq && ci < chunks) ? query[(int64_t)(q0 + qq) * chunks + ci]
+                                                     : make_uint4(0, 0, 0, 0);
+        }
+
+    const int64_t tile0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t tile1 = min(n, tile0 + rows_per_block);
+    for (int64_t base = tile0 + (int64_t)wave * RB; base < tile1; base += 4 * RB) {
+        uint4 v[RB][CPL];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                const int ci = lane + c * kWave;
+                const int64_t row = base + rb;
+                v[rb][c] = (row < tile1 && ci < chunks) ? B[row * chunks + ci] : make_uint4(0, 0, 0, 0);
+            }
+        float part[NQB * RB];
+#pragma unroll
+        for (int qq = 0; qq < NQB; ++qq)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                float s = 0.f;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) s += dot16(v[rb][c], qr[qq][c], Tag{});
+                part[qq * RB + rb] = s;
+            }
+        int which;
+        const float tot = wave_multi_sum<NQB * RB>(part, lane, &which);
+        constexpr int kLowBits = (NQB * RB >= 64) ? 0 : 6 - __builtin_ctz(NQB * RB);
+        if ((lane & ((1 << kLowBits) - 1)) == 0) {
+            const int qq = which / RB, rb = which % RB;
+            const int64_t row = base + rb;
+            if (row < tile1 && q0 + qq < nq) scores[(int64_t)(q0 + qq) * n + row] = tot;
+        }
+    }
+}
+
+template <class Tag, int CPL, int NQB>
+static hipError_t launch_scan_t(const void* query, const void* bank, int64_t n, int chunks, int nq,
+                                int64_t bank_stride_chunks, float* scores, hipStream_t st) {
+    constexpr int RB = (CPL <= 2) ? 4 : (CPL <= 4 ? 2 : 1);
+    const int groups = bank_stride_chunks ? nq : (nq + NQB - 1) / NQB;
+    // aim for >= ~2048 blocks in flight over the whole grid
+    int64_t rpb = (n * groups + 2047) / 2048;
+    rpb = ((rpb + 4 * RB - 1) / (4 * RB)) * (4 * RB);
+    if (rpb < 4 * RB) rpb = 4 * RB;
+    if (rpb > 1024) rpb = 1024;
+    const int64_t gx = (n + rpb - 1) / rpb;
+    dim3 grid((unsigned)gx, (unsigned)groups);
+    hipLaunchKernelGGL((scan_kernel<Tag, CPL, NQB, RB>), grid, dim3(256), 0, st,
+                       (const uint4*)query, (const uint4*)bank, n, chunks, nq, bank_stride_chunks,
+                       (int)rpb, scores);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, int nq,
+                       int64_t bank_stride, int dtype, float* scores, hipStream_t st) {
+    const int esz = dtype == 0 ? 4 : 2;
+    const int chunks = d * esz / 16;
+    const int64_t bsc = bank_stride * esz / 16;
+    const int cpl = (chunks + kWave - 1) / kWave;
+    // A shared bank serves several queries per block so each loaded row is
+    // reused from registers: 8 queries while a row takes <= 2 loads per lane,
+    // 4 while it takes <= 4; beyond that one query per block.
+    const bool multi = bsc == 0 && nq > 1;
+#define IS_SCAN(TAG)                                                                          \
+    do {                                                                                      \
+        if (multi && cpl <= 1) return launch_scan_t<TAG, 1, 8>(query, bank, n, chunks, nq, bsc, scores, st); \
+        if (multi && cpl <= 2) return launch_scan_t<TAG, 2, 8>(query, bank, n, chunks, nq, bsc, scores, st); \
+        if (multi && cpl <= 3) return launch_scan_t<TAG, 3, 4>(query, bank, n, chunks, nq, bsc, scores, st); \
+        if (multi && cpl <= 4) return launch_scan_t<TAG, 4, 4>(query, bank, n, chunks, nq, bsc, scores, st); \
+        if (cpl <= 1) return launch_scan_t<TAG, 1, 1>(query, bank, n, chunks, nq, bsc, scores, st);          \
+        if (cpl <= 2) return launch_scan_t<TAG, 2, 1>(query, bank, n, chunks, nq, bsc, scores, st);          \
+        if (cpl <= 3) return launch_scan_t<TAG, 3, 1>(query, bank, n, chunks, nq, bsc, scores, st);          \
+        if (cpl <= 4) return launch_scan_t<TAG, 4, 1>(query, bank, n, chunks, nq, bsc, scores, st);          \
+        if (cpl <= 8) return launch_scan_t<TAG, 8, 1>(query, bank, n, chunks, nq, bsc, scores, st);          \
+        return launch_scan_t<TAG, 16, 1>(query, bank, n, chunks, nq, bsc, scores, st);                       \
+    } while (0)
+    if (dtype == 0) IS_SCAN(F32Tag);
+    IS_SCAN(BF16Tag);
+#undef IS_SCAN
+}
+
+// ---- select ------------------------------------------------------------------
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelKpt = 16;
+
+// Block-wide OR / counts use these small shared arrays.
+struct SelShared {
+    uint32_t hist[256];
+    uint64_t wave_or[kSelThreads / kWave];
+    uint64_t first;
+    uint32_t digit;
+    uint32_t above;
+    uint32_t count;
+    uint64_t sel[IS_MAX_K];
+};
+
+__device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        uint32_t lo = __shfl_xor((uint32_t)v, off, kWave);
+        uint32_t hi = __shfl_xor((uint32_t)(v >> 32), off, kWave);
+        v |= ((uint64_t)hi << 32) | lo;
+    }
+    return v;
+}
+
+// FROM_SCORES: input is fp32 scores [nq][M] and the key id is the index.
+// Otherwise input is candidate keys [nq][M]; key 0 marks an empty entry.
+template <bool FROM_SCORES>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores,
+                                                             const uint64_t* __restrict__ keys_in,
+                                                             int64_t M, int k, int nchunks,
+                                                             uint64_t* __restrict__ cand_out,
+                                                             int32_t* __restrict__ out_ids,
+                                                             float* __restrict__ out_scores) {
+    __shared__ SelShared sh;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int q = blockIdx.y;
+    const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
+    const int64_t base = c0 + (int64_t)t * kSelKpt;
+
+    uint64_t key[kSelKpt];
+#pragma unroll
+    for (int i = 0; i < kSelKpt; ++i) {
+        const int64_t idx = base + i;
+        uint64_t kv = 0;
+        if (idx < M) {
+            if (FROM_SCORES)
+                kv = rank_key(scores[(int64_t)q * M + idx], (uint32_t)idx);
+            else
+                kv = keys_in[(int64_t)q * M + idx];
+        }
+        key[i] = kv;
+    }
+    // valid keys are nonzero: ~id has its top bit set for every id < 2^31
+    int nvalid = 0;
+#pragma unroll
+    for (int i = 0; i < kSelKpt; ++i) nvalid += key[i] != 0;
+
+    // block totals: count of valid keys and OR of (key ^ first valid key)
+    if (t == 0) { sh.count = 0; sh.first = 0; }
+    __syncthreads();
+    atomicAdd(&sh.count, (uint32_t)nvalid);
+    if (nvalid && key[0] != 0 && t == 0) sh.first = key[0];
+    __syncthreads();
+    if (sh.first == 0) {
+        // no key at the block's first slot: take any valid key
+        for (int i = 0; i < kSelKpt; ++i)
+            if (key[i] != 0) { atomicCAS((unsigned long long*)&sh.first, 0ull, (unsigned long long)key[i]); break; }
+        __syncthreads();
+    }
+    const uint32_t valid_total = sh.count;
+    const uint64_t first = sh.first;
+    const int want = (int)min<int64_t>(k, valid_total);
+
+    uint64_t diff = 0;
+#pragma unroll
+    for (int i = 0; i < kSelKpt; ++i)
+        if (key[i] != 0) diff |= key[i] ^ first;
+    diff = wave_or64(diff);
+    if (lane == 0) sh.wave_or[wave] = diff;
+    __syncthreads();
+    diff = 0;
+#pragma unroll
+    for (int w = 0; w < kSelThreads / kWave; ++w) diff |= sh.wave_or[w];
+
+    // radix select: after the loop every valid key with (key & pmask) >=
+    // prefix is selected, and exactly `want` keys qualify
+    uint64_t pmask = 0, prefix = 0;
+    if (want < (int)valid_total && diff != 0) {
+        int hi = 63 - __builtin_clzll(diff);
+        pmask = hi == 63 ? 0ull : ~((1ull << (hi + 1)) - 1);
+        prefix = first & pmask;
+        uint32_t remaining = (uint32_t)want;
+        while (true) {
+            const int lo = max(0, hi - 7);
+            const int width = hi - lo + 1;
+            const uint32_t dmask = (1u << width) - 1u;
+            if (t < 256) sh.hist[t] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < kSelKpt; ++i)
+                if (key[i] != 0 && (key[i] & pmask) == prefix)
+                    atomicAdd(&sh.hist[(uint32_t)(key[i] >> lo) & dmask], 1u);
+            __syncthreads();
+            if (wave == 0) {
+                // suffix sums over the 256 bins: lane L owns bins 4L..4L+3
+                uint32_t b0 = sh.hist[4 * lane], b1 = sh.hist[4 * lane + 1];
+                uint32_t b2 = sh.hist[4 * lane + 2], b3 = sh.hist[4 * lane + 3];
+                uint32_t mine = b0 + b1 + b2 + b3;
+                uint32_t incl = mine;  // sum over lanes >= lane
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    uint32_t o = __shfl_down(incl, off, kWave);
+                    if (lane + off < 64) incl += o;
+                }
+                uint32_t above = incl - mine;  // bins of higher lanes
+                // walk this lane's bins from the top
+                uint32_t a3 = above, a2 = a3 + b3, a1 = a2 + b2, a0 = a1 + b1;
+                if (a3 < remaining && remaining <= a3 + b3) { sh.digit = 4 * lane + 3; sh.above = a3; }
+                if (a2 < remaining && remaining <= a2 + b2) { sh.digit = 4 * lane + 2; sh.above = a2; }
+                if (a1 < remaining && remaining <= a1 + b1) { sh.digit = 4 * lane + 1; sh.above = a1; }
+                if (a0 < remaining && remaining <= a0 + b0) { sh.digit = 4 * lane; sh.above = a0; }
+            }
+            __syncthreads();
+            const uint32_t dg = sh.digit;
+            remaining -= sh.above;
+            const uint32_t inbin = sh.hist[dg];
+            prefix |= (uint64_t)dg << lo;
+            pmask |= (uint64_t)dmask << lo;
+            __syncthreads();  // hist is rewritten next pass
+            if (inbin == remaining || lo == 0) break;
+            hi = lo - 1;
+        }
+    }
+
+    // compaction of the selected keys into shared memory
+    if (t == 0) sh.count = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSelKpt; ++i)
+        if (key[i] != 0 && (key[i] & pmask) >= prefix) {
+            const uint32_t pos = atomicAdd(&sh.count, 1u);
+            if (pos < (uint32_t)k) sh.sel[pos] = key[i];
+        }
+    __syncthreads();
+    for (int i = want + t; i < k; i += kSelThreads) sh.sel[i] = 0;  // short chunk
+    __syncthreads();
+
+    if (out_ids) {
+        // final: order the k winners by rank (keys are distinct)
+        for (int i = t; i < k; i += kSelThreads) {
+            const uint64_t me = sh.sel[i];
+            int rank = 0;
+            for (int j = 0; j < k; ++j) rank += sh.sel[j] > me;
+            out_ids[(int64_t)q * k + rank] = (int32_t)key_id(me);
+            if (out_scores) out_scores[(int64_t)q * k + rank] = key_score(me);
+        }
+    } else {
+        uint64_t* dst = cand_out + ((int64_t)q * nchunks + blockIdx.x) * k;
+        for (int i = t; i < k; i += kSelThreads) dst[i] = sh.sel[i];
+    }
+}
+
+int64_t select_chunk_len() { return (int64_t)kSelThreads * kSelKpt; }
+
+hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
+                                uint64_t* cand, int32_t* out_ids, float* out_scores,
+                                hipStream_t st) {
+    dim3 grid((unsigned)nchunks, (unsigned)nq);
+    hipLaunchKernelGGL((select_kernel<true>), grid, dim3(kSelThreads), 0, st, scores,
+                       (const uint64_t*)nullptr, n, k, nchunks, cand, out_ids, out_scores);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, int nchunks,
+                              uint64_t* cand, int32_t* out_ids, float* out_scores, hipStream_t st) {
+    dim3 grid((unsigned)nchunks, (unsigned)nq);
+    hipLaunchKernelGGL((select_kernel<false>), grid, dim3(kSelThreads), 0, st,
+                       (const float*)nullptr, keys, M, k, nchunks, cand, out_ids, out_scores);
+    return hipGetLastError();
+}
+
+}  // namespace is

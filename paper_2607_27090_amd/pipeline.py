@@ -1,0 +1,68 @@
+"""Device buffers and call sequencing for one retrieve -> slot map -> inject
+pass (plumbing around the three C-ABI calls; no arithmetic of the path lives
+here)."""
+from __future__ import annotations
+
+import torch
+
+from . import (IS_DTYPE_BF16, IS_DTYPE_F32, is_inject, is_retrieve,
+               is_retrieve_workspace_size, is_slot_map)
+
+
+class RequestBuffers:
+    """Outputs and scratch of a batch of nq requests, allocated once.
+
+    ids/scores [nq][k], slots/positions [nq][max_tokens], m [nq], status [1]
+    and the retrieval workspace, all on ``device``."""
+
+    def __init__(self, *, n: int, d: int, k: int, nq: int, emb_dtype: torch.dtype,
+                 max_tokens: int, device="cuda"):
+        dt = IS_DTYPE_F32 if emb_dtype == torch.float32 else IS_DTYPE_BF16
+        self.n, self.d, self.k, self.nq, self.max_tokens = n, d, k, nq, max_tokens
+        ws = is_retrieve_workspace_size(n, d, k, nq, dt)
+        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        self.ids = torch.empty(nq, k, dtype=torch.int32, device=device)
+        self.scores = torch.empty(nq, k, dtype=torch.float32, device=device)
+        self.slots = torch.full((nq, max(max_tokens, 1)), -1, dtype=torch.int64, device=device)
+        self.positions = torch.full((nq, max(max_tokens, 1)), -1, dtype=torch.int32, device=device)
+        self.m = torch.zeros(nq, dtype=torch.int32, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def retrieve(self, query, bank, *, bank_stride=0, stream=None):
+        is_retrieve(query, bank, self.n, self.d, self.k, self.ids, self.scores, nq=self.nq,
+                    bank_stride=bank_stride, workspace=self.workspace, stream=stream)
+
+    def slot_map(self, fact_lens, start_pos, block_table, page_size, *, lens_stride,
+                 reverse_rank=1, stream=None):
+        is_slot_map(self.ids, fact_lens, start_pos, block_table, page_size, self.slots,
+                    self.positions, self.m, k=self.k, nq=self.nq, n=self.n,
+                    lens_stride=lens_stride, max_blocks=block_table.shape[-1],
+                    max_tokens=self.max_tokens, reverse_rank=reverse_rank, status=self.status,
+                    stream=stream)
+
+    def inject(self, preK, V, rope_theta, paged_k, paged_v, *, fact_offsets, fact_lens,
+               lens_stride, reverse_rank=1, stream=None):
+        L, T_store, H, D = preK.shape
+        is_inject(self.ids, preK, V, self.slots, self.positions, rope_theta, paged_k, paged_v,
+                  fact_offsets=fact_offsets, fact_lens=fact_lens, m=self.m, k=self.k,
+                  nq=self.nq, n=self.n, lens_stride=lens_stride, reverse_rank=reverse_rank,
+                  max_tokens=self.max_tokens, L=L, H=H, D=D, T_store=T_store,
+                  num_slots=paged_k.shape[1], status=self.status, stream=stream)
+
+
+def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, paged_v, *,
+                start_pos, page_size, rope_theta, shared_bank=True, reverse_rank=1,
+                stream=None):
+    """Enqueue retrieve -> slot map -> inject for every request of ``buf``.
+
+    ``store`` is a dict with preK, V ([L][T_store][H][D] bf16), fact_lens
+    ([banks][n] int32) and fact_offsets ([banks][n] int64)."""
+    n, d = buf.n, buf.d
+    bank_stride = 0 if shared_bank else n * d
+    lens_stride = 0 if store["fact_lens"].shape[0] == 1 else n
+    buf.retrieve(query, bank, bank_stride=bank_stride, stream=stream)
+    buf.slot_map(store["fact_lens"], start_pos, block_table, page_size, lens_stride=lens_stride,
+                 reverse_rank=reverse_rank, stream=stream)
+    buf.inject(store["preK"], store["V"], rope_theta, paged_k, paged_v,
+               fact_offsets=store["fact_offsets"], fact_lens=store["fact_lens"],
+               lens_stride=lens_stride, reverse_rank=reverse_rank, stream=stream)
