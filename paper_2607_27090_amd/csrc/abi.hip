@@ -65,6 +65,24 @@ int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dt
 
 }  // namespace
 
+namespace is {
+
+int compute_units() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        cached[dev] = cus;
+    }
+    return cached[dev];
+}
+
+}  // namespace is
+
 extern "C" {
 
 const char* is_version(void) { return "inferscale-gfx950 0.1.0"; }

@@ -12,15 +12,17 @@
 //     one wave covers one full (token, layer) row of H*D elements when
 //     H*D == 1024, i.e. 2 KiB of K and 2 KiB of V, read and written as whole
 //     128-byte lines;
-//   * a work unit is (256 consecutive thread items, a group of layers): the
-//     8 angles of a thread depend only on the token's position, so their
-//     fp64 reduction and fp32 sincos are paid once per unit and reused for
-//     every layer of the group;
-//   * the grid is persistent over work units and reads m from device memory,
-//     so the launch shape is fixed by max_tokens and a whole request can be
-//     enqueued (or captured in a graph) with no host round trip;
-//   * layers are processed UNROLL at a time so each thread keeps
-//     4 * UNROLL independent 16-byte loads in flight.
+//   * a work unit is (256 consecutive thread items, one layer), ordered token
+//     block first; every block of a fixed, persistent grid (~4 per CU, set by
+//     max_tokens only) takes one contiguous, equal share of its request's
+//     units, reading m from device memory, so a request can be enqueued (or
+//     captured in a graph) with no host round trip and no tail imbalance;
+//   * the 8 angles of a thread depend only on its token's position, so their
+//     fp64 reduction and fp32 sincos are paid once per token block of the
+//     share and reused for every layer in it;
+//   * layers are processed kUnroll at a time with unconditional loads, so
+//     each thread keeps 4 * kUnroll independent 16-byte loads in flight and
+//     the staging stays in registers.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -57,7 +59,7 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     const int64_t* __restrict__ fact_offsets, const int32_t* __restrict__ fact_lens,
     const int32_t* __restrict__ m_dev, int32_t k, int64_t n, int64_t lens_stride,
     int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
-    int64_t num_slots, int32_t layers_per_group, int32_t num_groups, uint32_t* __restrict__ status) {
+    int64_t num_slots, uint32_t* __restrict__ status) {
     __shared__ int64_t s_b[IS_MAX_K + 1];     // placed-token offset of each fact
     __shared__ int64_t s_off[IS_MAX_K];       // store row of each fact, -1: skip
     __shared__ double s_invf[IS_MAX_HEAD_DIM / 2];
@@ -72,10 +74,6 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     if (m <= 0) return;
     const int lpu = D >> 4;              // lane units per head
     const int U = H * lpu;               // lane units per (token, layer) row
-    const int64_t items = (int64_t)m * U;
-    const int64_t ntb = (items + kInjThreads - 1) / kInjThreads;
-    const int64_t units = ntb * num_groups;
-    if ((int64_t)blockIdx.x >= units) return;
 
     // ---- per-request setup: placement offsets, store rows, frequencies ----
     if (t == 0) { s_flags = 0; s_bad = 0; }
@@ -144,16 +142,24 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     // never place more tokens than the facts hold, whatever m says
     if ((int64_t)m > s_b[k]) m = (int32_t)s_b[k];
     const int64_t items_ok = (int64_t)m * U;
-    const int64_t units_ok = ((items_ok + kInjThreads - 1) / kInjThreads) * num_groups;
 
     const int64_t row_units = (int64_t)H * D / 8;  // 16-byte units per (token, layer) row
     const int64_t* slots_r = slots + (int64_t)r * max_tokens;
     const int32_t* pos_r = positions + (int64_t)r * max_tokens;
     const int half_units = D >> 4;                 // 16-byte units in half a head
 
-    for (int64_t u = blockIdx.x; u < units_ok; u += gridDim.x) {
-        const int64_t tb = u / num_groups;
-        const int g = (int)(u - tb * num_groups);
+    // Work units are (token block of kInjThreads items, layer), token-block
+    // major. Each block takes one contiguous, equal share of the units, so
+    // consecutive units usually share a token block and its angles.
+    const int64_t ntb_ok = (items_ok + kInjThreads - 1) / kInjThreads;
+    const int64_t total = ntb_ok * L;
+    const int64_t u0 = total * blockIdx.x / gridDim.x;
+    const int64_t u1 = total * (blockIdx.x + 1) / gridDim.x;
+    for (int64_t u = u0; u < u1;) {
+        const int64_t tb = u / L;
+        const int l0 = (int)(u - tb * L);
+        const int l1 = (int)min<int64_t>(L, l0 + (u1 - u));
+        u += l1 - l0;
         const int64_t item = tb * kInjThreads + t;
         if (item >= items_ok) continue;
         const int32_t token = (int32_t)(item / U);
@@ -187,30 +193,34 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
         }
 
         const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
-        const int l0 = g * layers_per_group;
-        const int l1 = min(L, l0 + layers_per_group);
+        const uint4* ksrc = preK + src * row_units + col;
+        const uint4* vsrc = V + src * row_units + col;
+        uint4* kdst = paged_k + slot * row_units + col;
+        uint4* vdst = paged_v + slot * row_units + col;
+        const int64_t sstride = T_store * row_units;    // one layer of the store
+        const int64_t dstride = num_slots * row_units;  // one layer of the pages
         for (int l = l0; l < l1; l += kUnroll) {
+            // loads are unconditional (a short tail re-reads its last layer)
+            // so the staging arrays stay in registers
             uint4 klo[kUnroll], khi[kUnroll], vlo[kUnroll], vhi[kUnroll];
 #pragma unroll
             for (int j = 0; j < kUnroll; ++j) {
-                if (l + j < l1) {
-                    const int64_t s_row = ((int64_t)(l + j) * T_store + src) * row_units + col;
-                    klo[j] = preK[s_row];
-                    khi[j] = preK[s_row + half_units];
-                    vlo[j] = V[s_row];
-                    vhi[j] = V[s_row + half_units];
-                }
+                const int64_t lj = min(l + j, l1 - 1);
+                klo[j] = ksrc[lj * sstride];
+                khi[j] = ksrc[lj * sstride + half_units];
+                vlo[j] = vsrc[lj * sstride];
+                vhi[j] = vsrc[lj * sstride + half_units];
             }
 #pragma unroll
             for (int j = 0; j < kUnroll; ++j) {
+                uint4 ylo, yhi;
+                rotate8(klo[j], khi[j], cs, sn, ylo, yhi);
                 if (l + j < l1) {
-                    const int64_t d_row = ((int64_t)(l + j) * num_slots + slot) * row_units + col;
-                    uint4 ylo, yhi;
-                    rotate8(klo[j], khi[j], cs, sn, ylo, yhi);
-                    paged_k[d_row] = ylo;
-                    paged_k[d_row + half_units] = yhi;
-                    paged_v[d_row] = vlo[j];
-                    paged_v[d_row + half_units] = vhi[j];
+                    const int64_t dj = (int64_t)(l + j) * dstride;
+                    kdst[dj] = ylo;
+                    kdst[dj + half_units] = yhi;
+                    vdst[dj] = vlo[j];
+                    vdst[dj + half_units] = vhi[j];
                 }
             }
         }
@@ -229,25 +239,18 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     const int64_t U = (int64_t)H * (D >> 4);
     const int64_t ntb_max = ((int64_t)max_tokens * U + kInjThreads - 1) / kInjThreads;
     if (ntb_max == 0) return hipSuccess;
-    // split layers into groups only as far as needed to give the chip
-    // enough work units; every group keeps >= 4 layers so the angle setup is
-    // amortised
-    const int64_t target_units = 2048;
-    int64_t groups = (target_units + ntb_max * nq - 1) / (ntb_max * nq);
-    const int64_t max_groups = L >= 4 ? L / 4 : 1;
-    if (groups > max_groups) groups = max_groups;
-    if (groups < 1) groups = 1;
-    const int lpg = (int)((L + groups - 1) / groups);
-    const int num_groups = (L + lpg - 1) / lpg;
-    int64_t per_req = ntb_max * num_groups;
-    const int64_t cap = (8192 + nq - 1) / nq;  // ~32 blocks per CU in total
-    if (per_req > cap) per_req = cap;
+    // a fixed, persistent grid of ~4 blocks per CU shared by the requests;
+    // each block takes an equal share of its request's (token block, layer)
+    // units, so the shape depends on max_tokens only, never on m
+    const int cus = compute_units();
+    int64_t per_req = (4LL * cus + nq - 1) / nq;
+    if (per_req > ntb_max * L) per_req = ntb_max * L;
+    if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
     hipLaunchKernelGGL(inject_kernel, grid, dim3(kInjThreads), 0, st, ids, (const uint4*)preK,
                        (const uint4*)V, slots, positions, rope_theta, (uint4*)paged_k,
                        (uint4*)paged_v, fact_offsets, fact_lens, m, k, n, lens_stride,
-                       reverse_rank, max_tokens, L, H, D, T_store, num_slots, lpg, num_groups,
-                       status);
+                       reverse_rank, max_tokens, L, H, D, T_store, num_slots, status);
     return hipGetLastError();
 }
 

@@ -10,6 +10,9 @@
 
 namespace is {
 
+// Compute units of the current device (cached per device; 256 on MI355X).
+int compute_units();
+
 // retrieve.hip
 hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, int nq,
                        int64_t bank_stride, int dtype, float* scores, hipStream_t st);

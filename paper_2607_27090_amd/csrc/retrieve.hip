@@ -7,12 +7,13 @@
 //     wave streams whole rows with 16-byte loads, keeps its queries in
 //     registers, and reduces per-row partial sums across the wave with a
 //     transposing butterfly so that V partial sums cost V-1 shuffles.
-//  2. select: radix select of the k largest 64-bit rank keys
-//     (score bits, ~id) per query. One 1024-thread workgroup owns a chunk of
-//     up to 16384 keys in registers; digits are taken 8 bits at a time from
-//     the highest bit in which the chunk's keys differ, until the boundary
-//     digit bucket is taken whole. Chunks emit k candidates each; a final
-//     pass over the candidates orders the winners (score desc, id asc).
+//  2. select: the k largest 64-bit rank keys (score bits, ~id) per query.
+//     One 1024-thread workgroup owns a chunk of up to 16384 keys in
+//     registers, bounds the answer from below by the per-wave c-th largest
+//     keys, and radix-selects among the few keys above that bound (8-bit
+//     digits from the highest differing bit). Chunks emit k candidates each;
+//     a final pass over the candidates orders the winners (score desc,
+//     id asc).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -175,29 +176,46 @@ hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, in
 constexpr int kSelThreads = 1024;
 constexpr int kSelKpt = 16;
 
-// Block-wide OR / counts use these small shared arrays.
 struct SelShared {
     uint32_t hist[256];
-    uint64_t wave_or[kSelThreads / kWave];
-    uint64_t first;
+    uint64_t wave_red[kSelThreads / kWave];
+    uint32_t count;
     uint32_t digit;
     uint32_t above;
-    uint32_t count;
     uint64_t sel[IS_MAX_K];
 };
 
-__device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int off) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, off, kWave);
+    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), off, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-        uint32_t lo = __shfl_xor((uint32_t)v, off, kWave);
-        uint32_t hi = __shfl_xor((uint32_t)(v >> 32), off, kWave);
-        v |= ((uint64_t)hi << 32) | lo;
+        const uint64_t o = shfl_xor64(v, off);
+        v = o > v ? o : v;
     }
     return v;
 }
 
-// FROM_SCORES: input is fp32 scores [nq][M] and the key id is the index.
-// Otherwise input is candidate keys [nq][M]; key 0 marks an empty entry.
+__device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v |= shfl_xor64(v, off);
+    return v;
+}
+
+// One block selects the `want` largest keys of a chunk of up to
+// kSelThreads * kSelKpt inputs (keys are distinct: the low word is ~id).
+//  1. Lower bound: every wave extracts its c-th largest key, c = ceil(want /
+//     #waves); the smallest of those, tau, has at least want keys >= it, so
+//     the answer lies among the keys >= tau (typically a few times want).
+//  2. Radix select over those candidates only, 8-bit digits from the highest
+//     bit in which they differ, until the boundary digit's bucket is taken
+//     whole.
+// FROM_SCORES: inputs are fp32 scores [nq][M] and a key's id is its index;
+// otherwise inputs are keys [nq][M] where 0 marks an empty entry.
 template <bool FROM_SCORES>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores,
                                                              const uint64_t* __restrict__ keys_in,
@@ -205,17 +223,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
                                                              uint64_t* __restrict__ cand_out,
                                                              int32_t* __restrict__ out_ids,
                                                              float* __restrict__ out_scores) {
+    constexpr int kWaves = kSelThreads / kWave;
     __shared__ SelShared sh;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int q = blockIdx.y;
     const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
-    const int64_t base = c0 + (int64_t)t * kSelKpt;
 
     uint64_t key[kSelKpt];
 #pragma unroll
     for (int i = 0; i < kSelKpt; ++i) {
-        const int64_t idx = base + i;
+        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
         uint64_t kv = 0;
         if (idx < M) {
             if (FROM_SCORES)
@@ -223,47 +241,76 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
             else
                 kv = keys_in[(int64_t)q * M + idx];
         }
-        key[i] = kv;
+        key[i] = kv;  // nonzero iff valid: ~id has its top bit set for ids < 2^31
     }
-    // valid keys are nonzero: ~id has its top bit set for every id < 2^31
     int nvalid = 0;
 #pragma unroll
     for (int i = 0; i < kSelKpt; ++i) nvalid += key[i] != 0;
-
-    // block totals: count of valid keys and OR of (key ^ first valid key)
-    if (t == 0) { sh.count = 0; sh.first = 0; }
+    if (t == 0) sh.count = 0;
     __syncthreads();
-    atomicAdd(&sh.count, (uint32_t)nvalid);
-    if (nvalid && key[0] != 0 && t == 0) sh.first = key[0];
+    if (nvalid) atomicAdd(&sh.count, (uint32_t)nvalid);
     __syncthreads();
-    if (sh.first == 0) {
-        // no key at the block's first slot: take any valid key
-        for (int i = 0; i < kSelKpt; ++i)
-            if (key[i] != 0) { atomicCAS((unsigned long long*)&sh.first, 0ull, (unsigned long long)key[i]); break; }
-        __syncthreads();
-    }
     const uint32_t valid_total = sh.count;
-    const uint64_t first = sh.first;
     const int want = (int)min<int64_t>(k, valid_total);
 
-    uint64_t diff = 0;
+    // ---- 1. candidate lower bound tau ----
+    uint64_t tau = 1;  // every valid key is >= 1
+    if (want < (int)valid_total) {
+        const int c = (want + kWaves - 1) / kWaves;
+        uint32_t removed = 0;
+        uint64_t kth = 0;
+        for (int round = 0; round < c; ++round) {
+            uint64_t best = 0;
+            int slot = -1;
+#pragma unroll
+            for (int i = 0; i < kSelKpt; ++i)
+                if (!(removed >> i & 1u) && key[i] > best) { best = key[i]; slot = i; }
+            const uint64_t wmax = wave_max64(best);
+            if (wmax != 0 && best == wmax && slot >= 0) removed |= 1u << slot;
+            kth = wmax;  // 0 once the wave runs out of keys
+        }
+        if (lane == 0) sh.wave_red[wave] = kth;
+        __syncthreads();
+        tau = ~0ull;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) tau = min(tau, sh.wave_red[w]);
+        if (tau == 0) tau = 1;
+        __syncthreads();  // wave_red is reused below
+    }
+
+    // ---- 2. radix select among candidates (key >= tau) ----
+    uint64_t pmask = 0, prefix = 0;
+    int ncand = 0;
+    uint64_t any = 0;
 #pragma unroll
     for (int i = 0; i < kSelKpt; ++i)
-        if (key[i] != 0) diff |= key[i] ^ first;
-    diff = wave_or64(diff);
-    if (lane == 0) sh.wave_or[wave] = diff;
+        if (key[i] >= tau) { ++ncand; any = key[i]; }
+    if (t == 0) sh.count = 0;
     __syncthreads();
-    diff = 0;
+    if (ncand) atomicAdd(&sh.count, (uint32_t)ncand);
+    // a reference candidate: the block-wide max (any candidate would do)
+    uint64_t ref = wave_max64(any);
+    if (lane == 0) sh.wave_red[wave] = ref;
+    __syncthreads();
+    const uint32_t cand_total = sh.count;
+    ref = 0;
 #pragma unroll
-    for (int w = 0; w < kSelThreads / kWave; ++w) diff |= sh.wave_or[w];
-
-    // radix select: after the loop every valid key with (key & pmask) >=
-    // prefix is selected, and exactly `want` keys qualify
-    uint64_t pmask = 0, prefix = 0;
-    if (want < (int)valid_total && diff != 0) {
-        int hi = 63 - __builtin_clzll(diff);
+    for (int w = 0; w < kWaves; ++w) ref = max(ref, sh.wave_red[w]);
+    __syncthreads();
+    if (want < (int)cand_total) {
+        uint64_t diff = 0;
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i)
+            if (key[i] >= tau) diff |= key[i] ^ ref;
+        diff = wave_or64(diff);
+        if (lane == 0) sh.wave_red[wave] = diff;
+        __syncthreads();
+        diff = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) diff |= sh.wave_red[w];
+        int hi = 63 - __builtin_clzll(diff | 1ull);
         pmask = hi == 63 ? 0ull : ~((1ull << (hi + 1)) - 1);
-        prefix = first & pmask;
+        prefix = ref & pmask;
         uint32_t remaining = (uint32_t)want;
         while (true) {
             const int lo = max(0, hi - 7);
@@ -273,23 +320,21 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
             __syncthreads();
 #pragma unroll
             for (int i = 0; i < kSelKpt; ++i)
-                if (key[i] != 0 && (key[i] & pmask) == prefix)
+                if (key[i] >= tau && (key[i] & pmask) == prefix)
                     atomicAdd(&sh.hist[(uint32_t)(key[i] >> lo) & dmask], 1u);
             __syncthreads();
             if (wave == 0) {
                 // suffix sums over the 256 bins: lane L owns bins 4L..4L+3
-                uint32_t b0 = sh.hist[4 * lane], b1 = sh.hist[4 * lane + 1];
-                uint32_t b2 = sh.hist[4 * lane + 2], b3 = sh.hist[4 * lane + 3];
-                uint32_t mine = b0 + b1 + b2 + b3;
+                const uint32_t b0 = sh.hist[4 * lane], b1 = sh.hist[4 * lane + 1];
+                const uint32_t b2 = sh.hist[4 * lane + 2], b3 = sh.hist[4 * lane + 3];
+                const uint32_t mine = b0 + b1 + b2 + b3;
                 uint32_t incl = mine;  // sum over lanes >= lane
 #pragma unroll
                 for (int off = 1; off < 64; off <<= 1) {
-                    uint32_t o = __shfl_down(incl, off, kWave);
+                    const uint32_t o = __shfl_down(incl, off, kWave);
                     if (lane + off < 64) incl += o;
                 }
-                uint32_t above = incl - mine;  // bins of higher lanes
-                // walk this lane's bins from the top
-                uint32_t a3 = above, a2 = a3 + b3, a1 = a2 + b2, a0 = a1 + b1;
+                const uint32_t a3 = incl - mine, a2 = a3 + b3, a1 = a2 + b2, a0 = a1 + b1;
                 if (a3 < remaining && remaining <= a3 + b3) { sh.digit = 4 * lane + 3; sh.above = a3; }
                 if (a2 < remaining && remaining <= a2 + b2) { sh.digit = 4 * lane + 2; sh.above = a2; }
                 if (a1 < remaining && remaining <= a1 + b1) { sh.digit = 4 * lane + 1; sh.above = a1; }
@@ -301,18 +346,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
             const uint32_t inbin = sh.hist[dg];
             prefix |= (uint64_t)dg << lo;
             pmask |= (uint64_t)dmask << lo;
-            __syncthreads();  // hist is rewritten next pass
+            __syncthreads();  // hist is rewritten by the next pass
             if (inbin == remaining || lo == 0) break;
             hi = lo - 1;
         }
     }
 
-    // compaction of the selected keys into shared memory
+    // ---- compaction of the selected keys ----
     if (t == 0) sh.count = 0;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kSelKpt; ++i)
-        if (key[i] != 0 && (key[i] & pmask) >= prefix) {
+        if (key[i] >= tau && (key[i] & pmask) >= prefix) {
             const uint32_t pos = atomicAdd(&sh.count, 1u);
             if (pos < (uint32_t)k) sh.sel[pos] = key[i];
         }

@@ -1,0 +1,127 @@
+"""CPU-only checks of the C ABI: the library loads, exports every entry point
+declared in include/inferscale.h, and rejects misuse on the host before
+anything is enqueued (no call here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_27090_amd as isl
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                   "inferscale.h")
+A = 1 << 20  # a 256-byte aligned fake device address (never dereferenced)
+
+
+def declared():
+    src = open(HDR).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(is_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_exported_set():
+    assert declared() == sorted(isl.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported():
+    lib = isl.load_library()
+    for name in declared():
+        assert hasattr(lib, name), name
+    assert isl.is_version().startswith("inferscale-gfx950")
+
+
+def _retrieve(**kw):
+    a = dict(q=A, bank=A, n=1000, d=64, k=10, ids=A, scores=A, nq=1, stride=0, dt=0, ws=A,
+             wsb=1 << 30, stream=None)
+    a.update(kw)
+    lib = isl.load_library()
+    return lib.is_retrieve(a["q"], a["bank"], a["n"], a["d"], a["k"], a["ids"], a["scores"],
+                           a["nq"], a["stride"], a["dt"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), isl.IS_ERR_INVALID),
+    (dict(bank=None), isl.IS_ERR_INVALID),
+    (dict(ids=None), isl.IS_ERR_INVALID),
+    (dict(k=0), isl.IS_ERR_INVALID),
+    (dict(k=1001), isl.IS_ERR_INVALID),
+    (dict(n=5000, k=1025), isl.IS_ERR_INVALID),
+    (dict(d=60), isl.IS_ERR_INVALID),
+    (dict(d=0), isl.IS_ERR_INVALID),
+    (dict(n=0), isl.IS_ERR_INVALID),
+    (dict(nq=0), isl.IS_ERR_INVALID),
+    (dict(dt=7), isl.IS_ERR_UNSUPPORTED),
+    (dict(stride=-8), isl.IS_ERR_INVALID),
+    (dict(stride=12), isl.IS_ERR_INVALID),
+    (dict(q=A + 4), isl.IS_ERR_INVALID),
+    (dict(bank=A + 8), isl.IS_ERR_INVALID),
+    (dict(ws=None), isl.IS_ERR_WORKSPACE),
+    (dict(wsb=16), isl.IS_ERR_WORKSPACE),
+    (dict(ws=A + 16), isl.IS_ERR_INVALID),
+])
+def test_retrieve_rejects(kw, code):
+    assert _retrieve(**kw) == code
+    assert isl.load_library().is_last_error().decode()
+
+
+def test_workspace_size_is_pure_host():
+    assert isl.is_retrieve_workspace_size(10000, 768, 50, 1) >= 10000 * 4
+    big = isl.is_retrieve_workspace_size(300000, 16, 1024, 1)
+    assert big >= 300000 * 4 + 2 * 19 * 1024 * 8
+    with pytest.raises(isl.InferScaleError):
+        isl.is_retrieve_workspace_size(10, 8, 11, 1)
+
+
+def _slot_map(**kw):
+    a = dict(ids=A, lens=A, start=0, bt=A, P=16, slots=A, pos=A, m=A, k=5, nq=1, n=100, ls=0,
+             mb=10, mt=100, rev=1, status=A)
+    a.update(kw)
+    return isl.load_library().is_slot_map(a["ids"], a["lens"], a["start"], a["bt"], a["P"],
+                                          a["slots"], a["pos"], a["m"], a["k"], a["nq"], a["n"],
+                                          a["ls"], a["mb"], a["mt"], a["rev"], a["status"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(ids=None), dict(lens=None), dict(bt=None), dict(slots=None), dict(pos=None),
+    dict(m=None), dict(k=0), dict(k=1025), dict(nq=0), dict(n=0), dict(P=0), dict(start=-1),
+    dict(mb=-1), dict(mt=-1), dict(start=2 ** 31 - 10), dict(ls=-1), dict(slots=A + 4),
+    dict(ids=A + 2), dict(status=A + 1),
+])
+def test_slot_map_rejects(kw):
+    assert _slot_map(**kw) == isl.IS_ERR_INVALID
+
+
+def _inject(**kw):
+    a = dict(ids=A, K=A, V=A, slots=A, pos=A, theta=500000.0, pk=A, pv=A, offs=A, lens=A, m=A,
+             k=5, nq=1, n=100, ls=0, rev=1, mt=100, L=2, H=8, D=128, T=1000, ns=1000, status=A)
+    a.update(kw)
+    return isl.load_library().is_inject(a["ids"], a["K"], a["V"], a["slots"], a["pos"],
+                                        a["theta"], a["pk"], a["pv"], a["offs"], a["lens"],
+                                        a["m"], a["k"], a["nq"], a["n"], a["ls"], a["rev"],
+                                        a["mt"], a["L"], a["H"], a["D"], a["T"], a["ns"],
+                                        a["status"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(ids=None), isl.IS_ERR_INVALID), (dict(K=None), isl.IS_ERR_INVALID),
+    (dict(V=None), isl.IS_ERR_INVALID), (dict(pk=None), isl.IS_ERR_INVALID),
+    (dict(m=None), isl.IS_ERR_INVALID), (dict(k=0), isl.IS_ERR_INVALID),
+    (dict(nq=0), isl.IS_ERR_INVALID), (dict(nq=70000), isl.IS_ERR_INVALID),
+    (dict(L=0), isl.IS_ERR_INVALID), (dict(H=0), isl.IS_ERR_INVALID),
+    (dict(D=15), isl.IS_ERR_UNSUPPORTED), (dict(D=24), isl.IS_ERR_UNSUPPORTED),
+    (dict(D=528), isl.IS_ERR_UNSUPPORTED), (dict(T=-1), isl.IS_ERR_INVALID),
+    (dict(theta=0.0), isl.IS_ERR_INVALID), (dict(theta=float("inf")), isl.IS_ERR_INVALID),
+    (dict(theta=float("nan")), isl.IS_ERR_INVALID), (dict(K=A + 8), isl.IS_ERR_INVALID),
+    (dict(pv=A + 4), isl.IS_ERR_INVALID), (dict(slots=A + 4), isl.IS_ERR_INVALID),
+])
+def test_inject_rejects(kw, code):
+    assert _inject(**kw) == code
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    t = torch.zeros(4, 8)
+    with pytest.raises(ValueError):
+        isl.is_retrieve(t, t, 4, 8, 1, torch.zeros(1, 1, dtype=torch.int32),
+                        workspace=torch.zeros(256, dtype=torch.uint8))
