@@ -176,13 +176,20 @@ hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, in
 constexpr int kSelThreads = 1024;
 constexpr int kSelKpt = 16;
 
+constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kSelCap = 2048;      // candidates kept in shared memory
+constexpr int kSelRankMax = 512;   // largest candidate set ranked pairwise
+
 struct SelShared {
+    uint64_t cand[kSelCap];
+    uint64_t group[IS_MAX_K];
+    uint64_t sel[IS_MAX_K];
     uint32_t hist[256];
-    uint64_t wave_red[kSelThreads / kWave];
+    uint32_t wcnt[kSelWaves];
+    uint64_t tau;
     uint32_t count;
     uint32_t digit;
     uint32_t above;
-    uint64_t sel[IS_MAX_K];
 };
 
 __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int off) {
@@ -191,11 +198,11 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int off) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
+__device__ __forceinline__ uint64_t wave_min64(uint64_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const uint64_t o = shfl_xor64(v, off);
-        v = o > v ? o : v;
+        v = o < v ? o : v;
     }
     return v;
 }
@@ -206,14 +213,22 @@ __device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
     return v;
 }
 
+// Lanes below this one whose bit is set in a wave-wide mask.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
 // One block selects the `want` largest keys of a chunk of up to
 // kSelThreads * kSelKpt inputs (keys are distinct: the low word is ~id).
-//  1. Lower bound: every wave extracts its c-th largest key, c = ceil(want /
-//     #waves); the smallest of those, tau, has at least want keys >= it, so
-//     the answer lies among the keys >= tau (typically a few times want).
-//  2. Radix select over those candidates only, 8-bit digits from the highest
-//     bit in which they differ, until the boundary digit's bucket is taken
-//     whole.
+//  1. Lower bound: thread t folds its keys' maximum into group t mod want;
+//     the smallest group maximum tau has at least `want` keys >= it (one per
+//     group), so the answer lies among the keys >= tau, typically a few
+//     times `want` of them.
+//  2. The candidates are compacted with wave ballots (no atomics) and, when
+//     few, ranked exactly by pairwise comparison, which also orders them;
+//     otherwise a radix select over the candidates picks the `want` largest
+//     (8-bit digits from the highest differing bit) and those are ranked.
 // FROM_SCORES: inputs are fp32 scores [nq][M] and a key's id is its index;
 // otherwise inputs are keys [nq][M] where 0 marks an empty entry.
 template <bool FROM_SCORES>
@@ -223,7 +238,6 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
                                                              uint64_t* __restrict__ cand_out,
                                                              int32_t* __restrict__ out_ids,
                                                              float* __restrict__ out_scores) {
-    constexpr int kWaves = kSelThreads / kWave;
     __shared__ SelShared sh;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
@@ -243,74 +257,103 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
         }
         key[i] = kv;  // nonzero iff valid: ~id has its top bit set for ids < 2^31
     }
-    int nvalid = 0;
+
+    // ---- valid count (wave ballots) ----
+    uint32_t wc = 0;
 #pragma unroll
-    for (int i = 0; i < kSelKpt; ++i) nvalid += key[i] != 0;
-    if (t == 0) sh.count = 0;
+    for (int i = 0; i < kSelKpt; ++i) wc += __popcll(__ballot(key[i] != 0));
+    if (lane == 0) sh.wcnt[wave] = wc;
+    for (int g = t; g < IS_MAX_K; g += kSelThreads) sh.group[g] = 0;
     __syncthreads();
-    if (nvalid) atomicAdd(&sh.count, (uint32_t)nvalid);
-    __syncthreads();
-    const uint32_t valid_total = sh.count;
+    uint32_t valid_total = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) valid_total += sh.wcnt[w];
     const int want = (int)min<int64_t>(k, valid_total);
 
-    // ---- 1. candidate lower bound tau ----
+    // ---- 1. lower bound tau ----
     uint64_t tau = 1;  // every valid key is >= 1
     if (want < (int)valid_total) {
-        const int c = (want + kWaves - 1) / kWaves;
-        uint32_t removed = 0;
-        uint64_t kth = 0;
-        for (int round = 0; round < c; ++round) {
-            uint64_t best = 0;
-            int slot = -1;
+        uint64_t tmax = 0;
 #pragma unroll
-            for (int i = 0; i < kSelKpt; ++i)
-                if (!(removed >> i & 1u) && key[i] > best) { best = key[i]; slot = i; }
-            const uint64_t wmax = wave_max64(best);
-            if (wmax != 0 && best == wmax && slot >= 0) removed |= 1u << slot;
-            kth = wmax;  // 0 once the wave runs out of keys
-        }
-        if (lane == 0) sh.wave_red[wave] = kth;
+        for (int i = 0; i < kSelKpt; ++i) tmax = key[i] > tmax ? key[i] : tmax;
+        if (tmax) atomicMax((unsigned long long*)&sh.group[t % want], (unsigned long long)tmax);
         __syncthreads();
-        tau = ~0ull;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) tau = min(tau, sh.wave_red[w]);
-        if (tau == 0) tau = 1;
-        __syncthreads();  // wave_red is reused below
+        if (wave == 0) {
+            uint64_t mn = ~0ull;
+            for (int g = lane; g < want; g += kWave) mn = min(mn, sh.group[g]);
+            mn = wave_min64(mn);
+            if (lane == 0) sh.tau = mn == 0 ? 1 : mn;  // an empty group: no filtering
+        }
+        __syncthreads();
+        tau = sh.tau;
     }
 
-    // ---- 2. radix select among candidates (key >= tau) ----
-    uint64_t pmask = 0, prefix = 0;
-    int ncand = 0;
-    uint64_t any = 0;
+    // ---- 2. candidates: keys >= tau, compacted by wave ballots ----
+    uint64_t mask[kSelKpt];
+    wc = 0;
 #pragma unroll
-    for (int i = 0; i < kSelKpt; ++i)
-        if (key[i] >= tau) { ++ncand; any = key[i]; }
-    if (t == 0) sh.count = 0;
+    for (int i = 0; i < kSelKpt; ++i) {
+        mask[i] = __ballot(key[i] >= tau);
+        wc += __popcll(mask[i]);
+    }
+    __syncthreads();  // wcnt reuse
+    if (lane == 0) sh.wcnt[wave] = wc;
     __syncthreads();
-    if (ncand) atomicAdd(&sh.count, (uint32_t)ncand);
-    // a reference candidate: the block-wide max (any candidate would do)
-    uint64_t ref = wave_max64(any);
-    if (lane == 0) sh.wave_red[wave] = ref;
-    __syncthreads();
-    const uint32_t cand_total = sh.count;
-    ref = 0;
+    uint32_t cand_total = 0, woff = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) ref = max(ref, sh.wave_red[w]);
-    __syncthreads();
-    if (want < (int)cand_total) {
-        uint64_t diff = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+        const uint32_t c = sh.wcnt[w];
+        woff += w < wave ? c : 0;
+        cand_total += c;
+    }
+    if (cand_total <= (uint32_t)kSelRankMax) {
+        uint32_t at = woff;
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            if (key[i] >= tau) sh.cand[at + lanes_below(mask[i])] = key[i];
+            at += __popcll(mask[i]);
+        }
+        __syncthreads();
+        // exact rank of every candidate (the number of larger candidates):
+        // S consecutive lanes share a candidate and split its comparisons
+        uint32_t S = 1;
+        while (S < 16 && 2 * S * cand_total <= (uint32_t)kSelThreads) S <<= 1;
+        const uint32_t part = (uint32_t)t & (S - 1);
+        for (uint32_t c = (uint32_t)t / S; c < cand_total; c += kSelThreads / S) {
+            const uint64_t me = sh.cand[c];
+            uint32_t rank = 0;
+            uint32_t j = part;
+            for (; j + 3 * S < cand_total; j += 4 * S)
+                rank += (sh.cand[j] > me) + (sh.cand[j + S] > me) + (sh.cand[j + 2 * S] > me) +
+                        (sh.cand[j + 3 * S] > me);
+            for (; j < cand_total; j += S) rank += sh.cand[j] > me;
+            for (uint32_t off = 1; off < S; off <<= 1) rank += __shfl_xor(rank, (int)off, kWave);
+            if (part == 0 && rank < (uint32_t)want) sh.sel[rank] = me;
+        }
+        __syncthreads();
+    } else {
+        // many candidates: radix select the `want` largest among them
+        uint64_t ref = 0, diff = 0;
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) ref = key[i] >= tau && key[i] > ref ? key[i] : ref;
+        if (t == 0) sh.tau = 0;
+        __syncthreads();
+        if (ref) atomicMax((unsigned long long*)&sh.tau, (unsigned long long)ref);
+        __syncthreads();
+        ref = sh.tau;  // the largest candidate
 #pragma unroll
         for (int i = 0; i < kSelKpt; ++i)
             if (key[i] >= tau) diff |= key[i] ^ ref;
         diff = wave_or64(diff);
-        if (lane == 0) sh.wave_red[wave] = diff;
+        __syncthreads();
+        if (lane == 0) sh.group[wave] = diff;
         __syncthreads();
         diff = 0;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) diff |= sh.wave_red[w];
+        for (int w = 0; w < kSelWaves; ++w) diff |= sh.group[w];
         int hi = 63 - __builtin_clzll(diff | 1ull);
-        pmask = hi == 63 ? 0ull : ~((1ull << (hi + 1)) - 1);
-        prefix = ref & pmask;
+        uint64_t pmask = hi == 63 ? 0ull : ~((1ull << (hi + 1)) - 1);
+        uint64_t prefix = ref & pmask;
         uint32_t remaining = (uint32_t)want;
         while (true) {
             const int lo = max(0, hi - 7);
@@ -350,33 +393,35 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
             if (inbin == remaining || lo == 0) break;
             hi = lo - 1;
         }
+        // the `want` winners, then their ranks among themselves
+        if (t == 0) sh.count = 0;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i)
+            if (key[i] >= tau && (key[i] & pmask) >= prefix) {
+                const uint32_t pos = atomicAdd(&sh.count, 1u);
+                if (pos < (uint32_t)want) sh.cand[pos] = key[i];
+            }
+        __syncthreads();
+        for (int c = t; c < want; c += kSelThreads) {
+            const uint64_t me = sh.cand[c];
+            int rank = 0;
+            for (int j = 0; j < want; ++j) rank += sh.cand[j] > me;
+            sh.sel[rank] = me;
+        }
+        __syncthreads();
     }
 
-    // ---- compaction of the selected keys ----
-    if (t == 0) sh.count = 0;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kSelKpt; ++i)
-        if (key[i] >= tau && (key[i] & pmask) >= prefix) {
-            const uint32_t pos = atomicAdd(&sh.count, 1u);
-            if (pos < (uint32_t)k) sh.sel[pos] = key[i];
-        }
-    __syncthreads();
-    for (int i = want + t; i < k; i += kSelThreads) sh.sel[i] = 0;  // short chunk
-    __syncthreads();
-
+    // ---- output, best first ----
     if (out_ids) {
-        // final: order the k winners by rank (keys are distinct)
-        for (int i = t; i < k; i += kSelThreads) {
+        for (int i = t; i < want; i += kSelThreads) {
             const uint64_t me = sh.sel[i];
-            int rank = 0;
-            for (int j = 0; j < k; ++j) rank += sh.sel[j] > me;
-            out_ids[(int64_t)q * k + rank] = (int32_t)key_id(me);
-            if (out_scores) out_scores[(int64_t)q * k + rank] = key_score(me);
+            out_ids[(int64_t)q * k + i] = (int32_t)key_id(me);
+            if (out_scores) out_scores[(int64_t)q * k + i] = key_score(me);
         }
     } else {
         uint64_t* dst = cand_out + ((int64_t)q * nchunks + blockIdx.x) * k;
-        for (int i = t; i < k; i += kSelThreads) dst[i] = sh.sel[i];
+        for (int i = t; i < k; i += kSelThreads) dst[i] = i < want ? sh.sel[i] : 0ull;
     }
 }
 
