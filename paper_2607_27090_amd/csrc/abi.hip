@@ -122,7 +122,9 @@ int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, i
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
     float* scores = (float*)(ws + lay.scores_off);
-    hipError_t e = is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
+    hipError_t e = is::scan_mfma_applies(n, d, nq, bank_stride, dtype)
+                       ? is::launch_scan_mfma(query_emb, bank, n, d, nq, scores, st)
+                       : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
     if (lay.nchunks == 1) {
         e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);

@@ -16,6 +16,9 @@ int compute_units();
 // retrieve.hip
 hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, int nq,
                        int64_t bank_stride, int dtype, float* scores, hipStream_t st);
+bool scan_mfma_applies(int64_t n, int d, int nq, int64_t bank_stride, int dtype);
+hipError_t launch_scan_mfma(const void* query, const void* bank, int64_t n, int d, int nq,
+                            float* scores, hipStream_t st);
 int64_t select_chunk_len();
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
                                 uint64_t* cand, int32_t* out_ids, float* out_scores,

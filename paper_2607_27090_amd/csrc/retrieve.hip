@@ -171,6 +171,137 @@ hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, in
 #undef IS_SCAN
 }
 
+// ---- batched scan on the matrix cores (many queries, one shared bf16 bank) ----
+//
+// Scores for nq queries against one bank form the product bank (n x d) times
+// queries^T (d x nq). A 512-thread block owns a tile of 256 bank rows x 256
+// queries; its 8 waves each accumulate 64 rows x 128 queries with
+// v_mfma_f32_32x32x16_bf16 (exact bf16 products, fp32 sums). The reduction
+// dimension advances in chunks of 64: each chunk of the bank tile (32 KiB)
+// and of the query tile (32 KiB) is staged in shared memory, double
+// buffered, with the next chunk's global loads in flight while the current
+// chunk feeds the matrix cores. Rows are 128 bytes in shared memory and the
+// eight 16-byte units of a row are XOR-swizzled by (row & 7), so the 32 rows
+// a fragment read touches fall in distinct banks.
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kMmRows = 256;     // bank rows per block
+constexpr int kMmQ = 256;        // queries per block
+constexpr int kMmK = 64;         // reduction chunk
+constexpr int kMmThreads = 512;  // 8 waves: 4 row groups x 2 query groups
+
+__global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(const uint4* __restrict__ bank,
+                                                               const uint4* __restrict__ query,
+                                                               int64_t n, int d, int nq,
+                                                               float* __restrict__ scores) {
+    __shared__ uint4 sA[2][kMmRows * 8];
+    __shared__ uint4 sB[2][kMmQ * 8];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int wr = wave & 3, wq = wave >> 2;
+    const int64_t row0 = (int64_t)blockIdx.x * kMmRows;
+    const int q0 = blockIdx.y * kMmQ;
+    const int units = d >> 3;                 // 16-byte units per row
+    const int nk = (d + kMmK - 1) / kMmK;
+
+    // this thread's 4 staging slots per operand: slot i = t + 512 j ->
+    // row i / 8, unit i % 8 of the chunk
+    uint4 ra[4], rb[4];
+    auto load_chunk = [&](int kc) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = t + kMmThreads * j;
+            const int r = i >> 3, u = i & 7;
+            const int gu = kc * 8 + u;
+            const int64_t row = row0 + r;
+            ra[j] = (row < n && gu < units) ? bank[row * units + gu] : make_uint4(0, 0, 0, 0);
+            const int q = q0 + r;
+            rb[j] = (q < nq && gu < units) ? query[(int64_t)q * units + gu] : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = t + kMmThreads * j;
+            const int r = i >> 3, u = i & 7;
+            sA[buf][r * 8 + (u ^ (r & 7))] = ra[j];
+            sB[buf][r * 8 + (u ^ (r & 7))] = rb[j];
+        }
+    };
+
+    f32x16_t acc[2][4];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = f32x16_t{};
+
+    load_chunk(0);
+    store_chunk(0);
+    __syncthreads();
+    for (int kc = 0; kc < nk; ++kc) {
+        const int buf = kc & 1;
+        if (kc + 1 < nk) load_chunk(kc + 1);
+#pragma unroll
+        for (int ks = 0; ks < kMmK / 16; ++ks) {
+            const int unit = ks * 2 + (lane >> 5);
+            bf16x8_t fa[2], fb[4];
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                const int r = wr * 64 + a * 32 + (lane & 31);
+                fa[a] = __builtin_bit_cast(bf16x8_t, sA[buf][r * 8 + (unit ^ (r & 7))]);
+            }
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int q = wq * 128 + b * 32 + (lane & 31);
+                fb[b] = __builtin_bit_cast(bf16x8_t, sB[buf][q * 8 + (unit ^ (q & 7))]);
+            }
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+        }
+        if (kc + 1 < nk) store_chunk(buf ^ 1);
+        __syncthreads();
+    }
+
+    // epilogue: lane holds query column (lane & 31) of each 32x32 tile and,
+    // for element e, row 8 (e / 4) + 4 (lane / 32) + e % 4
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int q = q0 + wq * 128 + b * 32 + (lane & 31);
+            if (q >= nq) continue;
+            float* out = scores + (int64_t)q * n;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int64_t row = row0 + wr * 64 + a * 32 + 8 * g + 4 * (lane >> 5);
+                const f32x16_t& v = acc[a][b];
+                if (row + 3 < n && (n & 3) == 0) {
+                    *(float4*)(out + row) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (row + e < n) out[row + e] = v[4 * g + e];
+                }
+            }
+        }
+}
+
+bool scan_mfma_applies(int64_t n, int d, int nq, int64_t bank_stride, int dtype) {
+    return dtype == IS_DTYPE_BF16 && bank_stride == 0 && nq >= 32 && d >= 64;
+}
+
+hipError_t launch_scan_mfma(const void* query, const void* bank, int64_t n, int d, int nq,
+                            float* scores, hipStream_t st) {
+    dim3 grid((unsigned)((n + kMmRows - 1) / kMmRows), (unsigned)((nq + kMmQ - 1) / kMmQ));
+    hipLaunchKernelGGL(scan_mfma_kernel, grid, dim3(kMmThreads), 0, st, (const uint4*)bank,
+                       (const uint4*)query, n, d, nq, scores);
+    return hipGetLastError();
+}
+
 // ---- select ------------------------------------------------------------------
 
 constexpr int kSelThreads = 1024;

@@ -36,6 +36,12 @@ def _ret_case(n, d, k, nq, dt, shared, seed):
     (777, 264, 7, 9, "bf16", True),          # ragged d, 9 queries over 2 groups
     (1000, 4096, 10, 2, "f32", True),        # long rows
     (3000, 8, 1, 4, "bf16", False),
+    # matrix-core scan (shared bf16 bank, >= 32 queries): ragged rows, ragged
+    # reduction chunks, partial query tiles and more queries than one tile
+    (1000, 64, 10, 32, "bf16", True),
+    (257, 72, 5, 33, "bf16", True),
+    (70000, 1024, 100, 100, "bf16", True),
+    (4099, 200, 64, 300, "bf16", True),
 ])
 def test_retrieve_shapes(n, d, k, nq, dt, shared):
     w = _ret_case(n, d, k, nq, dt, shared, seed=n % 97)
@@ -68,6 +74,20 @@ def test_retrieve_exact_ties_go_to_lower_id():
     buf.retrieve(q, bank)
     torch.cuda.synchronize()
     assert buf.ids[0, :5].tolist() == [3, 5, 9, 3000, 3999]
+
+
+def test_retrieve_exact_ties_matrix_core_path():
+    w = _ret_case(5000, 256, 8, 64, "bf16", True, seed=2)
+    bank = workloads.make_bank(w, "cuda")
+    for j in (17, 900, 4999):
+        bank[j] = bank[11]
+    q = workloads.make_queries(w, "cuda")
+    q[5] = bank[11]
+    buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype, max_tokens=1)
+    buf.retrieve(q, bank)
+    torch.cuda.synchronize()
+    assert buf.ids[5, :4].tolist() == [11, 17, 900, 4999]
+    assert len(set(buf.scores[5, :4].tolist())) == 1
 
 
 def test_retrieve_signed_zero_scores_tie():
