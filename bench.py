@@ -1,15 +1,20 @@
 """Benchmark of the InferScale serving-time hot path on one MI355X.
 
-One step = one request on the Llama-3.1-8B-shaped workload: exact top-k
-(k=50) over a 10,000-fact fp32 embedding bank (d=768), placement + slot map,
-and the fused gather + RoPE + scatter of the chosen facts' bf16 K/V
-(32 layers, 8 KV heads, head dim 128) into a paged cache with 16-token pages.
-Every step uses a different query (so different facts) and a different
-region of the page pool, with all inputs already resident in HBM.
+Default (the headline): one step = one request on the Llama-3.1-8B-shaped
+workload: exact top-k (k=50) over a 10,000-fact fp32 embedding bank
+(d=768), placement + slot map, and the fused gather + RoPE + scatter of the
+chosen facts' bf16 K/V (32 layers, 8 KV heads, head dim 128) into a paged
+cache with 16-token pages. Every step uses a different query (so different
+facts) and a different region of the page pool; all inputs are resident in
+HBM before the timed region starts.
 
-Prints one JSON line: µs per request (median over steps of the whole-step
-time is reported separately; `value` is total time / steps), the inject
-kernel's achieved HBM bandwidth against the 8 TB/s peak, and the CPU oracle
+--workload selects one of the other seeded shapes (64 users with their own
+banks, Llama-3-70B-style KV with 8 queries, a 1M-fact bf16 bank with 256
+queries); there a step is one batch of nq requests and `value` is the step
+time divided by nq.
+
+Prints one JSON line with µs per request, the inject kernel's achieved HBM
+bandwidth against the 8 TB/s peak, and (default workload) the CPU oracle
 timed on the host cores for a bounded sample of the same requests.
 """
 from __future__ import annotations
@@ -26,6 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def log(msg):
@@ -37,8 +43,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--k", type=int, default=50)
-    ap.add_argument("--regions", type=int, default=8, help="page-pool regions rotated over steps")
+    ap.add_argument("--workload", default="llama8b",
+                    choices=["llama8b", "tiny", "concurrency", "llama70b", "retrieval1m"])
+    ap.add_argument("--k", type=int, default=None, help="override k (llama8b sweep)")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -54,32 +61,64 @@ def main():
 
     import torch
     import workloads
-    from paper_2607_27090_amd.pipeline import RequestBuffers, run_request
+    from paper_2607_27090_amd import is_inject, is_slot_map
+    from paper_2607_27090_amd.pipeline import RequestBuffers
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda"
-    w = workloads.LLAMA8B.with_(k=args.k)
+    w = {"llama8b": workloads.LLAMA8B, "tiny": workloads.TINY,
+         "concurrency": workloads.CONCURRENCY, "llama70b": workloads.LLAMA70B,
+         "retrieval1m": workloads.RETRIEVAL1M}[args.workload]
+    if args.k is not None:
+        w = w.with_(k=args.k)
     nsteps = args.warmup + args.steps
+    # requests per slot-map/inject call: the whole batch, except the 1M-fact
+    # case whose 256 requests' pages would not fit at once
+    wave = 64 if w.nq > 64 else w.nq
+    nwaves = w.nq // wave
 
     t0 = time.time()
     bank = workloads.make_bank(w, dev)
     store = workloads.make_store(w, dev)
     queries = torch.stack([workloads.make_queries(w, dev, variant=i) for i in range(nsteps)])
-    R = args.regions
-    mb = w.max_blocks
-    bts, num_blocks = workloads.make_block_tables(w.with_(nq=R), dev, variant=0)
+    region_bytes = 2 * int(1.1 * wave * w.max_blocks) * w.page_size * w.L * w.H * w.D * 2
+    R = max(1, min(8, int(60e9 // region_bytes)))
+    bts, num_blocks = workloads.make_block_tables(w.with_(nq=R * wave), dev, variant=0)
+    bts = bts.view(R, wave, -1)
     pk, pv, num_slots = workloads.make_pages(w, num_blocks, dev)
-    buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=1, emb_dtype=bank.dtype,
+    buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
                          max_tokens=w.max_tokens, device=dev)
+    lens, offs = store["fact_lens"], store["fact_offsets"]
+    lens_stride = 0 if lens.shape[0] == 1 else w.n
+    L, T, H, D = store["preK"].shape
     torch.cuda.synchronize()
-    log(f"setup {time.time() - t0:.1f}s: store T={store['T_store']} rows "
-        f"({2 * store['preK'].numel() * 2 / 1e9:.1f} GB), pages {num_slots} slots x{R} regions")
+    log(f"setup {time.time() - t0:.1f}s: {w.name}, store T={T} rows "
+        f"({2 * store['preK'].numel() * 2 / 1e9:.1f} GB), pages {num_slots} slots, {R} regions")
+
+    def place(i, j):
+        sl = slice(j * wave, (j + 1) * wave)
+        ls = lens if lens_stride == 0 else lens[sl]
+        is_slot_map(buf.ids[sl], ls, w.start_pos, bts[(i * nwaves + j) % R], w.page_size,
+                    buf.slots[sl], buf.positions[sl], buf.m[sl], k=w.k, nq=wave, n=w.n,
+                    lens_stride=lens_stride, max_blocks=bts.shape[-1], max_tokens=w.max_tokens,
+                    status=buf.status)
+
+    def inject(j):
+        sl = slice(j * wave, (j + 1) * wave)
+        ls = lens if lens_stride == 0 else lens[sl]
+        os_ = offs if lens_stride == 0 else offs[sl]
+        is_inject(buf.ids[sl], store["preK"], store["V"], buf.slots[sl], buf.positions[sl],
+                  w.theta, pk, pv, fact_offsets=os_, fact_lens=ls, m=buf.m[sl], k=w.k, nq=wave,
+                  n=w.n, lens_stride=lens_stride, max_tokens=w.max_tokens, L=L, H=H, D=D,
+                  T_store=T, num_slots=num_slots, status=buf.status)
 
     def step(i):
-        run_request(buf, queries[i], bank, store, bts[i % R:i % R + 1], pk, pv,
-                    start_pos=w.start_pos, page_size=w.page_size, rope_theta=w.theta)
+        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        for j in range(nwaves):
+            place(i, j)
+            inject(j)
 
-    # ---- official timed region: K whole requests ------------------------------
+    # ---- official timed region: K steps -----------------------------------------
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -93,66 +132,74 @@ def main():
     wall = time.perf_counter() - t_host
     total_ms = ev0.elapsed_time(ev1)
     ms_per_step = total_ms / args.steps
-    log(f"timed {args.steps} requests: {total_ms:.3f} ms GPU ({wall * 1e3:.3f} ms host wall)")
+    log(f"timed {args.steps} steps: {total_ms:.3f} ms GPU ({wall * 1e3:.3f} ms host wall)")
 
-    # ---- instrumented pass: per-kernel events on the launch stream -------------
-    per = {"retrieve": [], "slot_map": [], "inject": [], "request": []}
-    evs = []
+    # ---- instrumented pass: per-call events on the launch stream ---------------
+    per = {"retrieve": [], "slot_map": [], "inject": [], "step": []}
+    recs = []
     for i in range(args.warmup, nsteps):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * nwaves)]
         e[0].record()
-        buf.retrieve(queries[i], bank)
+        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
         e[1].record()
-        buf.slot_map(store["fact_lens"], w.start_pos, bts[i % R:i % R + 1], w.page_size,
-                     lens_stride=0)
-        e[2].record()
-        buf.inject(store["preK"], store["V"], w.theta, pk, pv, fact_offsets=store["fact_offsets"],
-                   fact_lens=store["fact_lens"], lens_stride=0)
-        e[3].record()
-        evs.append(e)
+        for j in range(nwaves):
+            place(i, j)
+            e[2 + 2 * j].record()
+            inject(j)
+            e[3 + 2 * j].record()
+        recs.append(e)
     torch.cuda.synchronize()
-    ms = []
-    for i, e in zip(range(args.warmup, nsteps), evs):
+    for e in recs:
         per["retrieve"].append(e[0].elapsed_time(e[1]))
-        per["slot_map"].append(e[1].elapsed_time(e[2]))
-        per["inject"].append(e[2].elapsed_time(e[3]))
-        per["request"].append(e[0].elapsed_time(e[3]))
-    # m per step (deterministic: re-run the placement untimed)
+        prev, sm, inj = e[1], 0.0, 0.0
+        for j in range(nwaves):
+            sm += prev.elapsed_time(e[2 + 2 * j])
+            inj += e[2 + 2 * j].elapsed_time(e[3 + 2 * j])
+            prev = e[3 + 2 * j]
+        per["slot_map"].append(sm)
+        per["inject"].append(inj)
+        per["step"].append(e[0].elapsed_time(e[-1]))
+    # placed tokens per step (deterministic: re-run the placement untimed)
     m_steps = []
     for i in range(args.warmup, nsteps):
-        buf.retrieve(queries[i], bank)
-        buf.slot_map(store["fact_lens"], w.start_pos, bts[i % R:i % R + 1], w.page_size,
-                     lens_stride=0)
-        m_steps.append(int(buf.m.item()))
+        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        tot = 0
+        for j in range(nwaves):
+            place(i, j)
+            tot += int(buf.m[j * wave:(j + 1) * wave].sum())
+        m_steps.append(tot)
     assert int(buf.status.item()) == 0, "device status flags raised"
     inj_bytes = [workloads.inject_algorithmic_bytes(w, m) for m in m_steps]
     inj_ms = statistics.fmean(per["inject"])
     achieved = statistics.fmean(inj_bytes) / (inj_ms * 1e-3) / 1e9
-    log("per-kernel mean us: " + ", ".join(f"{k} {statistics.fmean(v) * 1e3:.1f}"
-                                         for k, v in per.items()))
-    log(f"inject: mean m={statistics.fmean(m_steps):.0f} tokens, "
-        f"{statistics.fmean(inj_bytes) / 1e6:.1f} MB/launch, {achieved:.0f} GB/s")
+    ret_ms = statistics.fmean(per["retrieve"])
+    scan_bytes = workloads.scan_algorithmic_bytes(w)
+    scan_flop = 2.0 * w.n * w.d_e * w.nq
+    log("per-call mean us: " + ", ".join(f"{k} {statistics.fmean(v) * 1e3:.1f}"
+                                       for k, v in per.items()))
+    log(f"inject: mean m={statistics.fmean(m_steps):.0f} tokens/step, "
+        f"{statistics.fmean(inj_bytes) / 1e6:.1f} MB/step, {achieved:.0f} GB/s")
 
     # ---- optional: the same request captured as a HIP graph --------------------
     graph_us = None
-    if args.graph:
+    if args.graph and nwaves == 1:
+        qbuf = queries[0].clone()
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
-        qbuf = queries[0].clone()
-        btbuf = bts[0:1].clone()
         with torch.cuda.stream(s):
-            run_request(buf, qbuf, bank, store, btbuf, pk, pv, start_pos=w.start_pos,
-                        page_size=w.page_size, rope_theta=w.theta)
+            buf.retrieve(qbuf, bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+            place(0, 0)
+            inject(0)
         torch.cuda.current_stream().wait_stream(s)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_request(buf, qbuf, bank, store, btbuf, pk, pv, start_pos=w.start_pos,
-                        page_size=w.page_size, rope_theta=w.theta)
+            buf.retrieve(qbuf, bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+            place(0, 0)
+            inject(0)
         torch.cuda.synchronize()
         times = []
         for i in range(args.warmup, nsteps):
             qbuf.copy_(queries[i])
-            btbuf.copy_(bts[i % R:i % R + 1])
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             g.replay()
@@ -160,7 +207,7 @@ def main():
             times.append((a, b))
         torch.cuda.synchronize()
         graph_us = statistics.median(a.elapsed_time(b) for a, b in times) * 1e3
-        log(f"graph replay median {graph_us:.1f} us/request")
+        log(f"graph replay median {graph_us:.1f} us/step")
 
     # ---- copy ceiling: a plain device-to-device copy of 1 GiB ------------------
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -177,12 +224,12 @@ def main():
 
     # ---- CPU baseline: the oracle on the host for a bounded sample ------------
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "llama8b":
         cpu = cpu_baseline(w, bank, store, queries, bts, args, torch)
 
     out = {
         "metric": "µs per request (retrieve+RoPE-inject) at k=50; inject HBM GB/s vs peak",
-        "value": round(ms_per_step * 1e3, 3),
+        "value": round(ms_per_step * 1e3 / w.nq, 3),
         "unit": "us/request",
         "n_gpus": 1,
         "steps": args.steps,
@@ -192,19 +239,24 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
-        "data": "synthetic (seeded N(0,1) bf16 pre-RoPE K/V, unit-norm fp32 embeddings)",
+        "data": "synthetic (seeded N(0,1) bf16 pre-RoPE K/V, unit-norm embeddings)",
         "config": {
-            "workload": (f"llama3.1-8b KV shapes (L={w.L}, H={w.H}, D={w.D}, bf16 KV), "
-                         f"n={w.n} facts of U[{w.len_lo},{w.len_hi}] tokens, d_e={w.d_e} fp32, "
-                         f"1 query, k={w.k}, page {w.page_size}, theta {w.theta:g}, "
+            "workload": (f"{w.name}: KV L={w.L} H={w.H} D={w.D} bf16; {w.n} facts per bank "
+                         f"({'shared' if w.shared_bank else 'one per request'}) of "
+                         f"U[{w.len_lo},{w.len_hi}] tokens; d_e={w.d_e} {w.emb_dtype}"
+                         f"{' clustered' if w.clustered else ''}; {w.nq} request(s) per step; "
+                         f"k={w.k}; page {w.page_size}; theta {w.theta:g}; "
                          f"start_pos {w.start_pos}"),
-            "k": w.k, "n": w.n, "nq": 1, "kv_dtype": "bf16", "emb_dtype": w.emb_dtype,
-            "mean_m_tokens": round(statistics.fmean(m_steps), 1),
+            "k": w.k, "n": w.n, "nq": w.nq, "kv_dtype": "bf16", "emb_dtype": w.emb_dtype,
+            "mean_m_tokens_per_step": round(statistics.fmean(m_steps), 1),
         },
-        "per_kernel_us": {k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()},
-        "request_us_median": round(statistics.median(per["request"]) * 1e3, 2),
-        "graph_request_us_median": None if graph_us is None else round(graph_us, 2),
+        "per_call_us": {k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()},
+        "step_us_median": round(statistics.median(per["step"]) * 1e3, 2),
+        "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),
+        "retrieve": {"us": round(ret_ms * 1e3, 2), "bank_bytes": scan_bytes,
+                     "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
+                     "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "roofline": {
             "bound": "hbm",
@@ -233,12 +285,13 @@ def cpu_baseline(w, bank, store, queries, bts, args, torch):
     lens = store["fact_lens"].cpu().numpy()
     offs = store["fact_offsets"].cpu().numpy()
     L, T, H, D = store["preK"].shape
+    R = bts.shape[0]
     done, spent, tokens = 0, 0.0, 0
     first = args.warmup
     while spent < args.cpu_seconds and first + done < args.warmup + args.steps:
         i = first + done
         q = queries[i].cpu().numpy()
-        bt = bts[i % args.regions:i % args.regions + 1].cpu().numpy()
+        bt = bts[i % R].cpu().numpy()
         # untimed: pull the rows the oracle will read into host memory
         ids_peek, _, _ = oracle.retrieve(q, bank_h, w.n, w.d_e, w.k)
         coffs = np.zeros_like(offs)
