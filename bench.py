@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--workload", default="llama8b",
                     choices=["llama8b", "tiny", "concurrency", "llama70b", "retrieval1m"])
     ap.add_argument("--k", type=int, default=None, help="override k (llama8b sweep)")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="HIP streams the requests are spread over (round robin)")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -86,53 +88,79 @@ def main():
     bts, num_blocks = workloads.make_block_tables(w.with_(nq=R * wave), dev, variant=0)
     bts = bts.view(R, wave, -1)
     pk, pv, num_slots = workloads.make_pages(w, num_blocks, dev)
-    buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
-                         max_tokens=w.max_tokens, device=dev)
+    S = max(1, args.streams)
+    bufs = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
+                           max_tokens=w.max_tokens, device=dev) for _ in range(S)]
+    buf = bufs[0]
     lens, offs = store["fact_lens"], store["fact_offsets"]
     lens_stride = 0 if lens.shape[0] == 1 else w.n
     L, T, H, D = store["preK"].shape
     torch.cuda.synchronize()
     log(f"setup {time.time() - t0:.1f}s: {w.name}, store T={T} rows "
         f"({2 * store['preK'].numel() * 2 / 1e9:.1f} GB), pages {num_slots} slots, {R} regions")
+    # requests that reuse a page region are always on the same stream
+    assert S == 1 or (nwaves == 1 and R % S == 0), "concurrent requests would share page regions"
 
-    def place(i, j):
+    def place(i, j, b=None):
+        b = buf if b is None else b
         sl = slice(j * wave, (j + 1) * wave)
         ls = lens if lens_stride == 0 else lens[sl]
-        is_slot_map(buf.ids[sl], ls, w.start_pos, bts[(i * nwaves + j) % R], w.page_size,
-                    buf.slots[sl], buf.positions[sl], buf.m[sl], k=w.k, nq=wave, n=w.n,
+        is_slot_map(b.ids[sl], ls, w.start_pos, bts[(i * nwaves + j) % R], w.page_size,
+                    b.slots[sl], b.positions[sl], b.m[sl], k=w.k, nq=wave, n=w.n,
                     lens_stride=lens_stride, max_blocks=bts.shape[-1], max_tokens=w.max_tokens,
-                    status=buf.status)
+                    status=b.status)
 
-    def inject(j):
+    def inject(j, b=None):
+        b = buf if b is None else b
         sl = slice(j * wave, (j + 1) * wave)
         ls = lens if lens_stride == 0 else lens[sl]
         os_ = offs if lens_stride == 0 else offs[sl]
-        is_inject(buf.ids[sl], store["preK"], store["V"], buf.slots[sl], buf.positions[sl],
-                  w.theta, pk, pv, fact_offsets=os_, fact_lens=ls, m=buf.m[sl], k=w.k, nq=wave,
+        is_inject(b.ids[sl], store["preK"], store["V"], b.slots[sl], b.positions[sl],
+                  w.theta, pk, pv, fact_offsets=os_, fact_lens=ls, m=b.m[sl], k=w.k, nq=wave,
                   n=w.n, lens_stride=lens_stride, max_tokens=w.max_tokens, L=L, H=H, D=D,
-                  T_store=T, num_slots=num_slots, status=buf.status)
+                  T_store=T, num_slots=num_slots, status=b.status)
 
-    def step(i):
-        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+    def step(i, b=None):
+        b = buf if b is None else b
+        b.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
         for j in range(nwaves):
-            place(i, j)
-            inject(j)
+            place(i, j, b)
+            inject(j, b)
+
+    main_stream = torch.cuda.current_stream()
+    streams = [main_stream] + [torch.cuda.Stream() for _ in range(S - 1)]
+
+    def timed(nstreams):
+        """K steps spread round robin over nstreams streams, bracketed by
+        events on the main stream that every other stream waits on and is
+        waited for."""
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(main_stream)
+        for s_ in streams[1:nstreams]:
+            s_.wait_event(ev0)
+        for i in range(args.warmup, nsteps):
+            si = (i - args.warmup) % nstreams
+            with torch.cuda.stream(streams[si]):
+                step(i, bufs[si])
+        for s_ in streams[1:nstreams]:
+            main_stream.wait_stream(s_)
+        ev1.record(main_stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1)
 
     # ---- official timed region: K steps -----------------------------------------
     for i in range(args.warmup):
-        step(i)
+        with torch.cuda.stream(streams[i % S]):
+            step(i, bufs[i % S])
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_host = time.perf_counter()
-    ev0.record()
-    for i in range(args.warmup, nsteps):
-        step(i)
-    ev1.record()
-    torch.cuda.synchronize()
+    total_ms = timed(S)
     wall = time.perf_counter() - t_host
-    total_ms = ev0.elapsed_time(ev1)
     ms_per_step = total_ms / args.steps
-    log(f"timed {args.steps} steps: {total_ms:.3f} ms GPU ({wall * 1e3:.3f} ms host wall)")
+    latency_ms = timed(1) / args.steps if S > 1 else ms_per_step
+    log(f"timed {args.steps} steps over {S} stream(s): {total_ms:.3f} ms GPU "
+        f"({wall * 1e3:.3f} ms host wall); one stream: {latency_ms * 1e3:.1f} us/step")
 
     # ---- instrumented pass: per-call events on the launch stream ---------------
     per = {"retrieve": [], "slot_map": [], "inject": [], "step": []}
@@ -251,6 +279,8 @@ def main():
             "mean_m_tokens_per_step": round(statistics.fmean(m_steps), 1),
         },
         "per_call_us": {k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()},
+        "streams": S,
+        "latency_us_per_step": round(latency_ms * 1e3, 3),
         "step_us_median": round(statistics.median(per["step"]) * 1e3, 2),
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),

@@ -69,16 +69,43 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
 
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r = blockIdx.y;
-    int32_t m = m_dev[r];
-    if (m > max_tokens) m = max_tokens;
+    const int32_t* rid = ids + (int64_t)r * k;
+    // issue the independent loads first: m, this thread's (up to 4) fact ids
+    // of the placement order, and below the first unit's slot and position
+    const int32_t m_in = m_dev[r];
+    int32_t cid[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = 4 * t + e;
+        cid[e] = i < k ? (reverse_rank ? rid[k - 1 - i] : rid[i]) : 0;
+    }
+    const int32_t m = min(m_in, max_tokens);
     if (m <= 0) return;
     const int lpu = D >> 4;              // lane units per head
     const int U = H * lpu;               // lane units per (token, layer) row
 
+    // Work units are (token block of kInjThreads items, layer), token-block
+    // major. Each block takes one contiguous, equal share of the units, so
+    // consecutive units usually share a token block and its angles.
+    const int64_t items = (int64_t)m * U;
+    const int64_t ntb = (items + kInjThreads - 1) / kInjThreads;
+    const int64_t total = ntb * L;
+    const int64_t u0 = total * blockIdx.x / gridDim.x;
+    const int64_t u1 = total * (blockIdx.x + 1) / gridDim.x;
+    const int64_t* slots_r = slots + (int64_t)r * max_tokens;
+    const int32_t* pos_r = positions + (int64_t)r * max_tokens;
+    const int64_t pf_tb = u0 < u1 ? u0 / L : -1;
+    int64_t pf_slot = -1;
+    int32_t pf_pos = 0;
+    if (pf_tb >= 0 && pf_tb * kInjThreads + t < items) {
+        const int64_t tok = (pf_tb * kInjThreads + t) / U;
+        pf_slot = slots_r[tok];
+        pf_pos = pos_r[tok];
+    }
+
     // ---- per-request setup: placement offsets, store rows, frequencies ----
     if (t == 0) { s_flags = 0; s_bad = 0; }
     __syncthreads();
-    const int32_t* rid = ids + (int64_t)r * k;
     const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
     const int64_t* offs = fact_offsets + (int64_t)r * lens_stride;
     // each thread owns up to 4 consecutive facts of the placement order
@@ -90,7 +117,7 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
         const int i = 4 * t + e;
         int32_t len = 0;
         if (i < k) {
-            const int32_t c = reverse_rank ? rid[k - 1 - i] : rid[i];
+            const int32_t c = cid[e];
             int64_t off = -1;
             if (c < 0 || (int64_t)c >= n) {
                 flags |= IS_DEV_ID_RANGE;
@@ -140,21 +167,11 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     }
     if (blockIdx.x != 0) flags = 0;  // fact-level flags are reported once per request
     // never place more tokens than the facts hold, whatever m says
-    if ((int64_t)m > s_b[k]) m = (int32_t)s_b[k];
-    const int64_t items_ok = (int64_t)m * U;
+    const int64_t items_ok = min(items, s_b[k] * U);
 
     const int64_t row_units = (int64_t)H * D / 8;  // 16-byte units per (token, layer) row
-    const int64_t* slots_r = slots + (int64_t)r * max_tokens;
-    const int32_t* pos_r = positions + (int64_t)r * max_tokens;
     const int half_units = D >> 4;                 // 16-byte units in half a head
 
-    // Work units are (token block of kInjThreads items, layer), token-block
-    // major. Each block takes one contiguous, equal share of the units, so
-    // consecutive units usually share a token block and its angles.
-    const int64_t ntb_ok = (items_ok + kInjThreads - 1) / kInjThreads;
-    const int64_t total = ntb_ok * L;
-    const int64_t u0 = total * blockIdx.x / gridDim.x;
-    const int64_t u1 = total * (blockIdx.x + 1) / gridDim.x;
     for (int64_t u = u0; u < u1;) {
         const int64_t tb = u / L;
         const int l0 = (int)(u - tb * L);
@@ -176,9 +193,9 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
         const int64_t off = s_off[lo];
         if (off < 0) continue;
         const int64_t src = off + (token - s_b[lo]);
-        const int64_t slot = slots_r[token];
+        const int64_t slot = tb == pf_tb ? pf_slot : slots_r[token];
         if (slot < 0 || slot >= num_slots) { flags |= IS_DEV_SLOT_RANGE; continue; }
-        const double p = (double)pos_r[token];
+        const double p = (double)(tb == pf_tb ? pf_pos : pos_r[token]);
 
         float cs[8], sn[8];
 #pragma unroll

@@ -7,13 +7,16 @@
 // the request is validated as a whole, then every placed token idx gets
 // position start_pos + idx and its slot from the block table. The slot of a
 // token depends only on its placed index, so no per-token fact lookup is
-// needed here.
+// needed, and the block-table entries are loaded at the start, alongside the
+// fact ids, instead of after the scan.
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace is {
 
 constexpr int kPlaceThreads = 1024;
+
+constexpr int kPlacePrefetch = 4;  // block-table entries each thread loads up front
 
 __global__ __launch_bounds__(kPlaceThreads) void slot_map_kernel(
     const int32_t* __restrict__ ids, const int32_t* __restrict__ fact_lens, int32_t start_pos,
@@ -29,13 +32,23 @@ __global__ __launch_bounds__(kPlaceThreads) void slot_map_kernel(
     const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
     const int32_t* bt = block_table + (int64_t)r * max_blocks;
 
+    // independent loads first: this thread's fact id and the block-table
+    // entries of the first placed tokens it will map (a token's slot depends
+    // only on its placed index, never on which fact it came from)
+    const int32_t c = t < k ? (reverse_rank ? rid[k - 1 - t] : rid[t]) : 0;
+    int32_t pb[kPlacePrefetch];
+#pragma unroll
+    for (int j = 0; j < kPlacePrefetch; ++j) {
+        const int64_t idx = t + (int64_t)j * kPlaceThreads;
+        const int64_t blk = ((int64_t)start_pos + idx) / page_size;
+        pb[j] = (idx < max_tokens && blk < max_blocks) ? bt[blk] : 0;
+    }
     if (t == 0) sflags = 0;
     __syncthreads();
 
     uint32_t flags = 0;
     int64_t len = 0;
     if (t < k) {
-        const int32_t c = reverse_rank ? rid[k - 1 - t] : rid[t];
         if (c < 0 || (int64_t)c >= n) {
             flags |= IS_DEV_ID_RANGE;
         } else {
@@ -60,11 +73,16 @@ __global__ __launch_bounds__(kPlaceThreads) void slot_map_kernel(
         if (f) atomicOr(&sflags, f);
     }
     __syncthreads();
-    if (sflags == 0 && total > 0) {
-        const int64_t b0 = start_pos / page_size;
-        const int64_t b1 = ((int64_t)start_pos + total - 1) / page_size;
-        for (int64_t b = b0 + t; b <= b1; b += kPlaceThreads)
-            if (bt[b] < 0) { atomicOr(&sflags, IS_DEV_BAD_BLOCK); break; }
+    if (sflags == 0) {
+        // every block the placement uses must be a real block
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < kPlacePrefetch; ++j)
+            if (t + (int64_t)j * kPlaceThreads < total && pb[j] < 0) bad = true;
+        for (int64_t idx = t + (int64_t)kPlacePrefetch * kPlaceThreads; idx < total;
+             idx += kPlaceThreads)
+            if (bt[((int64_t)start_pos + idx) / page_size] < 0) bad = true;
+        if (bad) atomicOr(&sflags, IS_DEV_BAD_BLOCK);
     }
     __syncthreads();
     const uint32_t req_flags = sflags;
@@ -77,10 +95,19 @@ __global__ __launch_bounds__(kPlaceThreads) void slot_map_kernel(
     }
     int64_t* slots_r = out_slots + (int64_t)r * max_tokens;
     int32_t* pos_r = out_positions + (int64_t)r * max_tokens;
-    for (int64_t idx = t; idx < total; idx += kPlaceThreads) {
+#pragma unroll
+    for (int j = 0; j < kPlacePrefetch; ++j) {
+        const int64_t idx = t + (int64_t)j * kPlaceThreads;
+        if (idx < total) {
+            const int64_t p = (int64_t)start_pos + idx;
+            slots_r[idx] = (int64_t)pb[j] * page_size + p % page_size;
+            pos_r[idx] = (int32_t)p;
+        }
+    }
+    for (int64_t idx = t + (int64_t)kPlacePrefetch * kPlaceThreads; idx < total;
+         idx += kPlaceThreads) {
         const int64_t p = (int64_t)start_pos + idx;
-        const int64_t blk = bt[p / page_size];
-        slots_r[idx] = blk * page_size + p % page_size;
+        slots_r[idx] = (int64_t)bt[p / page_size] * page_size + p % page_size;
         pos_r[idx] = (int32_t)p;
     }
     if (t == 0) out_m[r] = (int32_t)total;
