@@ -46,8 +46,10 @@ def parse():
     ap.add_argument("--workload", default="llama8b",
                     choices=["llama8b", "tiny", "concurrency", "llama70b", "retrieval1m"])
     ap.add_argument("--k", type=int, default=None, help="override k (llama8b sweep)")
-    ap.add_argument("--streams", type=int, default=2,
+    ap.add_argument("--streams", type=int, default=1,
                     help="HIP streams the requests are spread over (round robin)")
+    ap.add_argument("--detail", action="store_true",
+                    help="also time one stream (latency) and each call separately")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -158,14 +160,38 @@ def main():
     total_ms = timed(S)
     wall = time.perf_counter() - t_host
     ms_per_step = total_ms / args.steps
-    latency_ms = timed(1) / args.steps if S > 1 else ms_per_step
     log(f"timed {args.steps} steps over {S} stream(s): {total_ms:.3f} ms GPU "
-        f"({wall * 1e3:.3f} ms host wall); one stream: {latency_ms * 1e3:.1f} us/step")
+        f"({wall * 1e3:.3f} ms host wall)")
 
-    # ---- instrumented pass: per-call events on the launch stream ---------------
+    # ---- inject kernel alone: the same K requests' injects back to back -------
+    # (their retrieval and slot maps are recomputed untimed into one buffer
+    # set per step, so only inject launches sit between the two events)
+    sets = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
+                           max_tokens=w.max_tokens, device=dev, workspace=buf.workspace)
+            for _ in range(args.steps)]
+    for si, i in enumerate(range(args.warmup, nsteps)):
+        sets[si].retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        for j in range(nwaves):
+            place(i, j, sets[si])
+    torch.cuda.synchronize()
+    ei0, ei1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ei0.record()
+    for si in range(args.steps):
+        for j in range(nwaves):
+            inject(j, sets[si])
+    ei1.record()
+    torch.cuda.synchronize()
+    inj_launch_ms = ei0.elapsed_time(ei1) / (args.steps * nwaves)
+    log(f"inject alone: {inj_launch_ms * 1e3:.1f} us per launch")
+    latency_ms = None
+    if args.detail and S > 1:
+        latency_ms = timed(1) / args.steps
+        log(f"one stream: {latency_ms * 1e3:.1f} us/step")
+
+    # ---- instrumented pass (--detail): per-call events, one stream --------------
     per = {"retrieve": [], "slot_map": [], "inject": [], "step": []}
     recs = []
-    for i in range(args.warmup, nsteps):
+    for i in (range(args.warmup, nsteps) if args.detail else ()):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * nwaves)]
         e[0].record()
         buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
@@ -187,26 +213,20 @@ def main():
         per["slot_map"].append(sm)
         per["inject"].append(inj)
         per["step"].append(e[0].elapsed_time(e[-1]))
-    # placed tokens per step (deterministic: re-run the placement untimed)
-    m_steps = []
-    for i in range(args.warmup, nsteps):
-        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
-        tot = 0
-        for j in range(nwaves):
-            place(i, j)
-            tot += int(buf.m[j * wave:(j + 1) * wave].sum())
-        m_steps.append(tot)
-    assert int(buf.status.item()) == 0, "device status flags raised"
+    # placed tokens per step
+    m_steps = [int(b.m.sum()) for b in sets]
+    assert all(int(b.status.item()) == 0 for b in sets + bufs), "device status flags raised"
     inj_bytes = [workloads.inject_algorithmic_bytes(w, m) for m in m_steps]
-    inj_ms = statistics.fmean(per["inject"])
-    achieved = statistics.fmean(inj_bytes) / (inj_ms * 1e-3) / 1e9
-    ret_ms = statistics.fmean(per["retrieve"])
+    # algorithmic bytes per inject launch / mean launch duration (timed region)
+    achieved = statistics.fmean(inj_bytes) / nwaves / (inj_launch_ms * 1e-3) / 1e9
+    ret_ms = statistics.fmean(per["retrieve"]) if per["retrieve"] else None
     scan_bytes = workloads.scan_algorithmic_bytes(w)
     scan_flop = 2.0 * w.n * w.d_e * w.nq
-    log("per-call mean us: " + ", ".join(f"{k} {statistics.fmean(v) * 1e3:.1f}"
-                                       for k, v in per.items()))
+    if args.detail:
+        log("per-call mean us: " + ", ".join(f"{k} {statistics.fmean(v) * 1e3:.1f}"
+                                           for k, v in per.items()))
     log(f"inject: mean m={statistics.fmean(m_steps):.0f} tokens/step, "
-        f"{statistics.fmean(inj_bytes) / 1e6:.1f} MB/step, {achieved:.0f} GB/s")
+        f"{statistics.fmean(inj_bytes) / 1e6:.1f} MB/step, {achieved:.0f} GB/s per launch")
 
     # ---- optional: the same request captured as a HIP graph --------------------
     graph_us = None
@@ -278,15 +298,17 @@ def main():
             "k": w.k, "n": w.n, "nq": w.nq, "kv_dtype": "bf16", "emb_dtype": w.emb_dtype,
             "mean_m_tokens_per_step": round(statistics.fmean(m_steps), 1),
         },
-        "per_call_us": {k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()},
         "streams": S,
-        "latency_us_per_step": round(latency_ms * 1e3, 3),
-        "step_us_median": round(statistics.median(per["step"]) * 1e3, 2),
+        "inject_launch_us": round(inj_launch_ms * 1e3, 2),
+        "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
+                        if args.detail else None),
+        "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),
-        "retrieve": {"us": round(ret_ms * 1e3, 2), "bank_bytes": scan_bytes,
-                     "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
-                     "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
+        "retrieve": None if ret_ms is None else {
+            "us": round(ret_ms * 1e3, 2), "bank_bytes": scan_bytes,
+            "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
+            "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "roofline": {
             "bound": "hbm",
@@ -295,11 +317,33 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if args.workload == "llama8b" and w.k == 50 else None,
+            "traffic_unit": "HBM bytes per launch (scaled FETCH_SIZE + WRITE_SIZE)",
+            "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves),
         },
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per inject launch from the committed counter summary, or
+    None when the kernel sources changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "inject_kernel_llama8b_k50_traffic.md")
+    csrc = os.path.join(ROOT, "paper_2607_27090_amd", "csrc")
+    try:
+        text = open(path).read()
+        tb = int(re.search(r"^traffic_bytes_per_launch: (\d+)", text, re.M).group(1))
+        want = dict(re.findall(r"(\S+\.h\w*) ([0-9a-f]{64})", text))
+    except (OSError, AttributeError):
+        return None
+    for name, digest in want.items():
+        with open(os.path.join(csrc, name), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
+    return tb if want else None
 
 
 def cpu_baseline(w, bank, store, queries, bts, args, torch):

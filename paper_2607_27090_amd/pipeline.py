@@ -16,11 +16,16 @@ class RequestBuffers:
     and the retrieval workspace, all on ``device``."""
 
     def __init__(self, *, n: int, d: int, k: int, nq: int, emb_dtype: torch.dtype,
-                 max_tokens: int, device="cuda"):
+                 max_tokens: int, device="cuda", workspace=None):
         dt = IS_DTYPE_F32 if emb_dtype == torch.float32 else IS_DTYPE_BF16
         self.n, self.d, self.k, self.nq, self.max_tokens = n, d, k, nq, max_tokens
         ws = is_retrieve_workspace_size(n, d, k, nq, dt)
-        self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        if workspace is not None:
+            # shared scratch: callers on one stream may reuse it in turn
+            assert workspace.numel() * workspace.element_size() >= ws
+            self.workspace = workspace
+        else:
+            self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
         self.ids = torch.empty(nq, k, dtype=torch.int32, device=device)
         self.scores = torch.empty(nq, k, dtype=torch.float32, device=device)
         self.slots = torch.full((nq, max(max_tokens, 1)), -1, dtype=torch.int64, device=device)
