@@ -172,11 +172,27 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     const int64_t row_units = (int64_t)H * D / 8;  // 16-byte units per (token, layer) row
     const int half_units = D >> 4;                 // 16-byte units in half a head
 
+    const int64_t sstride = T_store * row_units;    // one layer of the store
+    const int64_t dstride = num_slots * row_units;  // one layer of the pages
+    // the slot and position of the next segment's token are loaded one
+    // segment ahead, so a segment switch does not wait on them
+    int64_t nx_slot = pf_slot;
+    int32_t nx_pos = pf_pos;
     for (int64_t u = u0; u < u1;) {
         const int64_t tb = u / L;
         const int l0 = (int)(u - tb * L);
         const int l1 = (int)min<int64_t>(L, l0 + (u1 - u));
         u += l1 - l0;
+        const int64_t slot_in = nx_slot;
+        const int32_t pos_in = nx_pos;
+        if (u < u1) {
+            const int64_t nitem = (u / L) * kInjThreads + t;
+            if (nitem < items_ok) {
+                const int64_t ntok = nitem / U;
+                nx_slot = slots_r[ntok];
+                nx_pos = pos_r[ntok];
+            }
+        }
         const int64_t item = tb * kInjThreads + t;
         if (item >= items_ok) continue;
         const int32_t token = (int32_t)(item / U);
@@ -193,29 +209,16 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
         const int64_t off = s_off[lo];
         if (off < 0) continue;
         const int64_t src = off + (token - s_b[lo]);
-        const int64_t slot = tb == pf_tb ? pf_slot : slots_r[token];
+        const int64_t slot = slot_in;
         if (slot < 0 || slot >= num_slots) { flags |= IS_DEV_SLOT_RANGE; continue; }
-        const double p = (double)(tb == pf_tb ? pf_pos : pos_r[token]);
-
-        float cs[8], sn[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            // angle p * w_j formed in fp64, reduced to [-pi, pi] with a
-            // two-constant 2*pi, then fp32 sine and cosine
-            const double a = p * s_invf[sub * 8 + e];
-            const double nrev = rint(a * 0.15915494309189535);
-            double red = fma(-nrev, 6.283185307179586, a);
-            red = fma(-nrev, 2.4492935982947064e-16, red);
-            sincosf((float)red, &sn[e], &cs[e]);
-        }
 
         const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
         const uint4* ksrc = preK + src * row_units + col;
         const uint4* vsrc = V + src * row_units + col;
         uint4* kdst = paged_k + slot * row_units + col;
         uint4* vdst = paged_v + slot * row_units + col;
-        const int64_t sstride = T_store * row_units;    // one layer of the store
-        const int64_t dstride = num_slots * row_units;  // one layer of the pages
+
+        float cs[8], sn[8];
         for (int l = l0; l < l1; l += kUnroll) {
             // loads are unconditional (a short tail re-reads its last layer)
             // so the staging arrays stay in registers
@@ -227,6 +230,20 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
                 khi[j] = ksrc[lj * sstride + half_units];
                 vlo[j] = vsrc[lj * sstride];
                 vhi[j] = vsrc[lj * sstride + half_units];
+            }
+            if (l == l0) {
+                // the segment's angles, computed while its first loads are in
+                // flight: p * w_j formed in fp64, reduced to [-pi, pi] with a
+                // two-constant 2*pi, then fp32 sine and cosine
+                const double p = (double)pos_in;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const double a = p * s_invf[sub * 8 + e];
+                    const double nrev = rint(a * 0.15915494309189535);
+                    double red = fma(-nrev, 6.283185307179586, a);
+                    red = fma(-nrev, 2.4492935982947064e-16, red);
+                    sincosf((float)red, &sn[e], &cs[e]);
+                }
             }
 #pragma unroll
             for (int j = 0; j < kUnroll; ++j) {
