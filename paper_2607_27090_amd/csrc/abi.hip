@@ -1,6 +1,7 @@
 // C ABI of libinferscale: host-side argument validation, workspace layout and
 // launch sequencing. The contract of every entry point is documented in
 // include/inferscale.h.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -52,6 +53,38 @@ RetrieveLayout retrieve_layout(int64_t n, int32_t k, int32_t nq) {
     return lay;
 }
 
+// Filtered matrix-core retrieval (many queries on one shared bf16 bank): the
+// scores of a sample of the first S rows [nq][S], the sample's winners
+// [nq][k], survivor counts [nq][G] and survivor regions [nq][G][rows per
+// block], where G * rows per block <= (n - S) + 32 G (G <= the block bound).
+struct FusedLayout {
+    size_t scores_off, first_off, counts_off, regions_off, total;
+    int64_t sample;
+};
+
+FusedLayout fused_layout(int64_t n, int32_t k, int32_t nq) {
+    FusedLayout lay{};
+    const int64_t S = is::select_chunk_len();
+    const int64_t gmax = is::mfma_max_blocks();
+    lay.sample = S;
+    size_t off = 0;
+    lay.scores_off = off;
+    off = round_up(off + (size_t)nq * S * sizeof(float), 256);
+    lay.first_off = off;
+    off = round_up(off + (size_t)nq * k * sizeof(uint64_t), 256);
+    lay.counts_off = off;
+    off = round_up(off + (size_t)nq * gmax * sizeof(uint32_t), 256);
+    lay.regions_off = off;
+    off = round_up(off + (size_t)nq * (size_t)(n - S + 32 * gmax) * sizeof(uint64_t), 256);
+    lay.total = off;
+    return lay;
+}
+
+// The sample pays off once the bank is well beyond one select chunk.
+bool fused_applies(int64_t n, int32_t d, int32_t nq, int64_t bank_stride, int32_t dtype) {
+    return is::scan_mfma_applies(n, d, nq, bank_stride, dtype) && n > 2 * is::select_chunk_len();
+}
+
 int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dtype) {
     if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
     if (d < 8 || d > 8192 || d % 8) return fail(IS_ERR_INVALID, "d=%d must be a multiple of 8 in [8, 8192]", d);
@@ -95,7 +128,10 @@ int is_retrieve_workspace_size(int64_t n, int32_t d, int32_t k, int32_t nq, int3
     *bytes = 0;
     const int rc = check_retrieve_sizes(n, d, k, nq, dtype);
     if (rc) return rc;
-    *bytes = retrieve_layout(n, k, nq).total;
+    size_t total = retrieve_layout(n, k, nq).total;
+    // the bank layout is not known here: cover the filtered path too
+    if (fused_applies(n, d, nq, 0, dtype)) total = std::max(total, fused_layout(n, k, nq).total);
+    *bytes = total;
     return ok();
 }
 
@@ -114,17 +150,45 @@ int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, i
     if (!aligned(out_ids, 4) || (out_scores && !aligned(out_scores, 4)))
         return fail(IS_ERR_INVALID, "out_ids/out_scores must be 4-byte aligned");
     const RetrieveLayout lay = retrieve_layout(n, k, nq);
-    if (!workspace || workspace_bytes < lay.total)
-        return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total,
+    const bool fused = fused_applies(n, d, nq, bank_stride, dtype);
+    const size_t need = fused ? fused_layout(n, k, nq).total : lay.total;
+    if (!workspace || workspace_bytes < need)
+        return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need,
                     workspace ? workspace_bytes : (size_t)0);
     if (!aligned(workspace, 256)) return fail(IS_ERR_INVALID, "workspace must be 256-byte aligned");
 
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
+    hipError_t e;
+    if (fused) {
+        // 1. dense scores of the first S rows; 2. their k winners, whose k-th
+        // key bounds the answer from below; 3. the rest of the bank keeps
+        // only keys above it; 4. exact ranking of sample winners + survivors
+        const FusedLayout fl = fused_layout(n, k, nq);
+        const int64_t S = fl.sample;
+        float* sc = (float*)(ws + fl.scores_off);
+        uint64_t* first = (uint64_t*)(ws + fl.first_off);
+        uint32_t* counts = (uint32_t*)(ws + fl.counts_off);
+        uint64_t* regions = (uint64_t*)(ws + fl.regions_off);
+        e = is::launch_scan_mfma(query_emb, bank, d, nq, 0, S, sc, S, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+        e = is::launch_select_scores(sc, S, k, nq, 1, first, nullptr, nullptr, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        e = is::launch_scan_mfma_filter(query_emb, bank, d, nq, S, n, first, k, regions, counts,
+                                        st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+        int G;
+        int64_t rpb;
+        is::mfma_grid(n - S, &G, &rpb);
+        e = is::launch_select_regions(first, regions, counts, G, rpb, k, nq, out_ids, out_scores,
+                                      st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        return ok();
+    }
     float* scores = (float*)(ws + lay.scores_off);
-    hipError_t e = is::scan_mfma_applies(n, d, nq, bank_stride, dtype)
-                       ? is::launch_scan_mfma(query_emb, bank, n, d, nq, scores, st)
-                       : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
+    e = is::scan_mfma_applies(n, d, nq, bank_stride, dtype)
+            ? is::launch_scan_mfma(query_emb, bank, d, nq, 0, n, scores, n, st)
+            : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
     if (lay.nchunks == 1) {
         e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);

@@ -27,6 +27,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
+// Integer minimum of two 64-bit values. (HIP's min() with mixed operand
+// types promotes both to double; these keep integer arithmetic.)
+__device__ __forceinline__ int64_t min_i64(int64_t a, int64_t b) { return a < b ? a : b; }
+
 // ---- ranking keys ----------------------------------------------------------
 // A 64-bit key whose unsigned order is the rank order (score desc, id asc):
 // high word = order-preserving image of the fp32 score (-0 folded onto +0,

@@ -181,7 +181,7 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     for (int64_t u = u0; u < u1;) {
         const int64_t tb = u / L;
         const int l0 = (int)(u - tb * L);
-        const int l1 = (int)min<int64_t>(L, l0 + (u1 - u));
+        const int l1 = (int)min_i64(L, l0 + (u1 - u));
         u += l1 - l0;
         const int64_t slot_in = nx_slot;
         const int32_t pos_in = nx_pos;

@@ -17,14 +17,28 @@ int compute_units();
 hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, int nq,
                        int64_t bank_stride, int dtype, float* scores, hipStream_t st);
 bool scan_mfma_applies(int64_t n, int d, int nq, int64_t bank_stride, int dtype);
-hipError_t launch_scan_mfma(const void* query, const void* bank, int64_t n, int d, int nq,
-                            float* scores, hipStream_t st);
+// Blocks and rows per block of a matrix-core scan over `rows` rows (at most
+// mfma_max_blocks() blocks; rows_per_block is a multiple of 32).
+void mfma_grid(int64_t rows, int* blocks, int64_t* rows_per_block);
+int mfma_max_blocks();
+// Dense scores of rows [row_begin, row_end): scores[q * ld + row - row_begin].
+hipError_t launch_scan_mfma(const void* query, const void* bank, int d, int nq, int64_t row_begin,
+                            int64_t row_end, float* scores, int64_t ld, hipStream_t st);
+// Keys above tau_keys[q * k + k - 1] of rows [row_begin, row_end), written to
+// regions[q][g][rows_per_block] with counts[q][g] (g < blocks of mfma_grid).
+hipError_t launch_scan_mfma_filter(const void* query, const void* bank, int d, int nq,
+                                   int64_t row_begin, int64_t row_end, const uint64_t* tau_keys,
+                                   int k, uint64_t* regions, uint32_t* counts, hipStream_t st);
 int64_t select_chunk_len();
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
                                 uint64_t* cand, int32_t* out_ids, float* out_scores,
                                 hipStream_t st);
 hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, int nchunks,
                               uint64_t* cand, int32_t* out_ids, float* out_scores, hipStream_t st);
+// Final ranking from the sample winners first[q][k] and the filter survivors.
+hipError_t launch_select_regions(const uint64_t* first, const uint64_t* regions,
+                                 const uint32_t* counts, int G, int64_t rcap, int k, int nq,
+                                 int32_t* out_ids, float* out_scores, hipStream_t st);
 
 // place.hip
 hipError_t launch_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,

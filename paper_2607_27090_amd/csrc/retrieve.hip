@@ -174,131 +174,291 @@ hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, in
 // ---- batched scan on the matrix cores (many queries, one shared bf16 bank) ----
 //
 // Scores for nq queries against one bank form the product bank (n x d) times
-// queries^T (d x nq). A 512-thread block owns a tile of 256 bank rows x 256
-// queries; its 8 waves each accumulate 64 rows x 128 queries with
-// v_mfma_f32_32x32x16_bf16 (exact bf16 products, fp32 sums). The reduction
+// queries^T (d x nq). A persistent 512-thread block owns one contiguous,
+// equal share of the bank rows and walks it in tiles of 256 rows x 256
+// queries; its 4 waves (one per SIMD, so each may hold 512 registers) each
+// accumulate 128 rows x 128 queries with v_mfma_f32_32x32x16_bf16 (exact bf16
+// products, fp32 sums). The reduction
 // dimension advances in chunks of 64: each chunk of the bank tile (32 KiB)
 // and of the query tile (32 KiB) is staged in shared memory, double
-// buffered, with the next chunk's global loads in flight while the current
-// chunk feeds the matrix cores. Rows are 128 bytes in shared memory and the
-// eight 16-byte units of a row are XOR-swizzled by (row & 7), so the 32 rows
-// a fragment read touches fall in distinct banks.
+// buffered. The bank is the only operand that comes from HBM (the query
+// tile stays in L2), so every thread keeps kMmDepth bank chunks in flight
+// in registers, and the pipeline runs on across tile boundaries. Rows are
+// 128 bytes in shared memory and the eight 16-byte units of a row are
+// XOR-swizzled by (row & 7), so the 32 rows a fragment read touches fall in
+// distinct banks.
+//
+// Two epilogues per finished tile:
+//  * dense: every score is stored, scores[q * ld + (row - row_begin)];
+//  * filter: only keys whose score is not below the score of a per-query
+//    threshold key tau_q are kept. tau_q is the k-th best key of a row sample,
+//    so every key of the exact top-k outside the sample is above it: the
+//    top-k of the sample's top-k plus these survivors is the exact top-k.
+//    Survivors of block g and query q go to their own region [q][g] of
+//    capacity rows_per_block, which cannot overflow.
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kMmRows = 256;     // bank rows per block
-constexpr int kMmQ = 256;        // queries per block
+constexpr int kMmRows = 256;     // bank rows per tile
+constexpr int kMmQ = 256;        // queries per tile
 constexpr int kMmK = 64;         // reduction chunk
-constexpr int kMmThreads = 512;  // 8 waves: 4 row groups x 2 query groups
+constexpr int kMmThreads = 256;  // 4 waves: 2 row groups x 2 query groups
+constexpr int kMmDepth = 2;      // chunks in flight per thread
+constexpr int kMmSlots = kMmRows * 8 / kMmThreads;  // 16-byte staging slots per thread
+constexpr int kMmMaxBlocks = 1024;
 
-__global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(const uint4* __restrict__ bank,
-                                                               const uint4* __restrict__ query,
-                                                               int64_t n, int d, int nq,
-                                                               float* __restrict__ scores) {
+// Raw buffer descriptors: loads at byte offsets >= the descriptor's size
+// read zero, which pads ragged row tiles and reduction chunks for free.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family raw buffer format word
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             kRsrcWord3);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(rsrc_t r, uint32_t off) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond any descriptor here (<= 4 MiB)
+
+template <bool FILTER>
+__global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
+    const uint4* __restrict__ bank, const uint4* __restrict__ query, int d, int nq,
+    int64_t row_begin, int64_t row_end, int64_t rows_per_block, float* __restrict__ scores,
+    int64_t ld, const uint64_t* __restrict__ tau_keys, int k, uint64_t* __restrict__ regions,
+    uint32_t* __restrict__ counts) {
     __shared__ uint4 sA[2][kMmRows * 8];
     __shared__ uint4 sB[2][kMmQ * 8];
+    __shared__ uint32_t s_cnt[FILTER ? kMmQ : 1];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int wr = wave & 3, wq = wave >> 2;
-    const int64_t row0 = (int64_t)blockIdx.x * kMmRows;
+    const int wr = wave & 1, wq = wave >> 1;
     const int q0 = blockIdx.y * kMmQ;
+    const int G = gridDim.x;
     const int units = d >> 3;                 // 16-byte units per row
-    const int nk = (d + kMmK - 1) / kMmK;
+    // reduction chunks per tile, padded to a multiple of the prefetch depth
+    // (padding chunks read as zero)
+    const int nk = ((d + kMmK - 1) / kMmK + kMmDepth - 1) / kMmDepth * kMmDepth;
+    const int64_t blk0 = row_begin + (int64_t)blockIdx.x * rows_per_block;
+    const int64_t blk1 = min(row_end, blk0 + rows_per_block);
 
-    // this thread's 4 staging slots per operand: slot i = t + 512 j ->
-    // row i / 8, unit i % 8 of the chunk
-    uint4 ra[4], rb[4];
-    auto load_chunk = [&](int kc) {
+    if (FILTER && t < kMmQ) s_cnt[t] = 0;
+    if (blk0 >= blk1) {
+        // an empty share still reports its (zero) survivor counts
+        if (FILTER && t < kMmQ && q0 + t < nq) counts[(int64_t)(q0 + t) * G + blockIdx.x] = 0;
+        return;
+    }
+    const int nrows = (int)(blk1 - blk0);  // rows of this block's share
+    const int ntiles = (nrows + kMmRows - 1) / kMmRows;
+    const int steps = ntiles * nk;  // (tile, chunk) pairs of this block, tile major
+
+    // staging slot i = t + kMmThreads j (j < kMmSlots) holds row i / 8 =
+    // t / 8 + 32 j, unit i % 8 = t % 8 of a chunk; bank and query tiles use
+    // the same offsets
+    constexpr int kRowStep = kMmThreads / 8;
+    const int r_t = t >> 3, u_t = t & 7;
+    auto chunk_off = [&](int kc, int j) -> uint32_t {
+        const int gu = kc * 8 + u_t;
+        return gu < units ? (uint32_t)(((r_t + kRowStep * j) * units + gu) * 16) : kOutOfRange;
+    };
+    const rsrc_t qsrc = make_rsrc(query + (int64_t)q0 * units,
+                                  (uint32_t)(min(nq - q0, kMmQ) * units * 16));
+    auto load_a = [&](int s, uint4 (&dst)[kMmSlots]) {
+        const int sc = min(s, steps - 1);
+        const int tile = sc / nk, kc = sc - tile * nk;
+        const int64_t r0 = blk0 + (int64_t)tile * kMmRows;
+        const int64_t rows = min_i64(blk1 - r0, kMmRows);
+        const rsrc_t asrc = make_rsrc(bank + r0 * units, (uint32_t)(rows * units * 16));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int i = t + kMmThreads * j;
-            const int r = i >> 3, u = i & 7;
-            const int gu = kc * 8 + u;
-            const int64_t row = row0 + r;
-            ra[j] = (row < n && gu < units) ? bank[row * units + gu] : make_uint4(0, 0, 0, 0);
-            const int q = q0 + r;
-            rb[j] = (q < nq && gu < units) ? query[(int64_t)q * units + gu] : make_uint4(0, 0, 0, 0);
+        for (int j = 0; j < kMmSlots; ++j) dst[j] = buffer_load16(asrc, chunk_off(kc, j));
+    };
+    auto load_b = [&](int s, uint4 (&dst)[kMmSlots]) {
+        const int kc = min(s, steps - 1) % nk;
+#pragma unroll
+        for (int j = 0; j < kMmSlots; ++j) dst[j] = buffer_load16(qsrc, chunk_off(kc, j));
+    };
+    auto store_chunk = [&](int buf, const uint4 (&a)[kMmSlots], const uint4 (&b)[kMmSlots]) {
+#pragma unroll
+        for (int j = 0; j < kMmSlots; ++j) {
+            const int r = r_t + kRowStep * j;
+            sA[buf][r * 8 + (u_t ^ (r & 7))] = a[j];
+            sB[buf][r * 8 + (u_t ^ (r & 7))] = b[j];
         }
     };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int i = t + kMmThreads * j;
-            const int r = i >> 3, u = i & 7;
-            sA[buf][r * 8 + (u ^ (r & 7))] = ra[j];
-            sB[buf][r * 8 + (u ^ (r & 7))] = rb[j];
-        }
-    };
 
-    f32x16_t acc[2][4];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = f32x16_t{};
+    f32x16_t acc[4][4];
 
-    load_chunk(0);
-    store_chunk(0);
-    __syncthreads();
-    for (int kc = 0; kc < nk; ++kc) {
-        const int buf = kc & 1;
-        if (kc + 1 < nk) load_chunk(kc + 1);
+    // every fragment row / column this lane reads is = lane (mod 8), so one
+    // swizzled unit offset per reduction step serves all of them
+    const uint4* pa = &sA[0][(wr * 128 + (lane & 31)) * 8];
+    const uint4* pb = &sB[0][(wq * 128 + (lane & 31)) * 8];
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int ks = 0; ks < kMmK / 16; ++ks) {
-            const int unit = ks * 2 + (lane >> 5);
-            bf16x8_t fa[2], fb[4];
+            const int off = buf * (kMmRows * 8) + ((ks * 2 + (lane >> 5)) ^ (lane & 7));
+            bf16x8_t fa[4], fb[4];
 #pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                const int r = wr * 64 + a * 32 + (lane & 31);
-                fa[a] = __builtin_bit_cast(bf16x8_t, sA[buf][r * 8 + (unit ^ (r & 7))]);
-            }
+            for (int a = 0; a < 4; ++a) fa[a] = __builtin_bit_cast(bf16x8_t, pa[a * 32 * 8 + off]);
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const int q = wq * 128 + b * 32 + (lane & 31);
-                fb[b] = __builtin_bit_cast(bf16x8_t, sB[buf][q * 8 + (unit ^ (q & 7))]);
-            }
+            for (int b = 0; b < 4; ++b) fb[b] = __builtin_bit_cast(bf16x8_t, pb[b * 32 * 8 + off]);
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int b = 0; b < 4; ++b)
                     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
         }
-        if (kc + 1 < nk) store_chunk(buf ^ 1);
-        __syncthreads();
+    };
+
+    // filter: the threshold scores of the lane's 4 query columns
+    float tau_s[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        const int q = q0 + wq * 128 + b * 32 + (lane & 31);
+        tau_s[b] = (FILTER && q < nq) ? key_score(tau_keys[(int64_t)q * k + (k - 1)]) : 0.f;
     }
 
-    // epilogue: lane holds query column (lane & 31) of each 32x32 tile and,
-    // for element e, row 8 (e / 4) + 4 (lane / 32) + e % 4
+    // epilogue of a finished tile: lane holds query column (lane & 31) of each
+    // 32x32 tile and, for element e, row 8 (e / 4) + 4 (lane / 32) + e % 4
+    auto epilogue = [&](int tile) {
+        const int64_t r0 = blk0 + (int64_t)tile * kMmRows;
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int q = q0 + wq * 128 + b * 32 + (lane & 31);
-            if (q >= nq) continue;
-            float* out = scores + (int64_t)q * n;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int64_t row = row0 + wr * 64 + a * 32 + 8 * g + 4 * (lane >> 5);
+            for (int b = 0; b < 4; ++b) {
+                const int qq = wq * 128 + b * 32 + (lane & 31);
+                const int q = q0 + qq;
                 const f32x16_t& v = acc[a][b];
-                if (row + 3 < n && (n & 3) == 0) {
-                    *(float4*)(out + row) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
-                } else {
+                if (FILTER) {
+                    // keep every key whose score is not below tau's: a superset
+                    // of the keys above tau (also when a score or tau is NaN),
+                    // and any superset of the top-k ranks to the same top-k.
+                    // The block maximum (NaN-ignoring) rules out a whole 32x32
+                    // block at once; a NaN score is only needed when tau is NaN.
+                    float mx = v[0];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (row + e < n) out[row + e] = v[4 * g + e];
+                    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, v[e]);
+                    if (!(mx < tau_s[b]) && q < nq) {
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) {
+                            const int rr = tile * kMmRows + wr * 128 + a * 32 + 8 * (e >> 2) +
+                                           4 * (lane >> 5) + (e & 3);  // row within the share
+                            if (!(v[e] < tau_s[b]) && rr < nrows) {
+                                // the region address is formed here only (the
+                                // empty asm keeps it from being hoisted into
+                                // registers live across the whole scan)
+                                int ql = q;
+                                asm volatile("" : "+v"(ql));
+                                uint64_t* reg =
+                                    regions + ((int64_t)ql * G + blockIdx.x) * rows_per_block;
+                                const uint32_t pos = atomicAdd(&s_cnt[qq], 1u);
+                                reg[pos] = rank_key(v[e], (uint32_t)(blk0 + rr));
+                            }
+                        }
+                    }
+                    // one 32x32 block at a time: keeps the accumulators from
+                    // being read out (and spilled) all at once
+                    __builtin_amdgcn_sched_barrier(0);
+                } else {
+                    if (q >= nq) continue;
+                    float* out = scores + (int64_t)q * ld - row_begin;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int64_t row = r0 + wr * 128 + a * 32 + 8 * g + 4 * (lane >> 5);
+                        if (row + 3 < blk1 && ((ld | (row - row_begin)) & 3) == 0) {
+                            *(float4*)(out + row) =
+                                make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (row + e < blk1) out[row + e] = v[4 * g + e];
+                        }
+                    }
                 }
             }
+    };
+
+    // pipeline over the block's (tile, chunk) steps s = tile * nk + chunk:
+    // chunk s is in shared memory while the bank and query parts of chunks
+    // s+1 .. s+kMmDepth are in flight in ra[] / rb[]. Loads complete in issue
+    // order, so both parts of a chunk are issued together, kMmDepth steps
+    // before they are staged. Chunk s lives in slot s % kMmDepth, and nk is a
+    // multiple of kMmDepth, so every register index is static.
+    uint4 ra[kMmDepth][kMmSlots], rb[kMmDepth][kMmSlots];
+#pragma unroll
+    for (int j = 0; j < kMmDepth; ++j) {
+        load_b(j, rb[j]);
+        load_a(j, ra[j]);
+    }
+    store_chunk(0, ra[0], rb[0]);
+    __syncthreads();
+    for (int tile = 0; tile < ntiles; ++tile) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) acc[a][b] = f32x16_t{};
+        for (int kc0 = 0; kc0 < nk; kc0 += kMmDepth) {
+#pragma unroll
+            for (int p = 0; p < kMmDepth; ++p) {
+                const int s = tile * nk + kc0 + p;
+                const int buf = s & 1;
+                load_b(s + kMmDepth, rb[p]);
+                load_a(s + kMmDepth, ra[p]);
+                compute(buf);
+                if (s + 1 < steps)
+                    store_chunk(buf ^ 1, ra[(p + 1) % kMmDepth], rb[(p + 1) % kMmDepth]);
+                __syncthreads();
+            }
         }
+        epilogue(tile);
+    }
+    if (FILTER) {
+        __syncthreads();  // every wave's survivors are counted
+        if (t < kMmQ && q0 + t < nq) counts[(int64_t)(q0 + t) * G + blockIdx.x] = s_cnt[t];
+    }
 }
 
 bool scan_mfma_applies(int64_t n, int d, int nq, int64_t bank_stride, int dtype) {
     return dtype == IS_DTYPE_BF16 && bank_stride == 0 && nq >= 32 && d >= 64;
 }
 
-hipError_t launch_scan_mfma(const void* query, const void* bank, int64_t n, int d, int nq,
-                            float* scores, hipStream_t st) {
-    dim3 grid((unsigned)((n + kMmRows - 1) / kMmRows), (unsigned)((nq + kMmQ - 1) / kMmQ));
-    hipLaunchKernelGGL(scan_mfma_kernel, grid, dim3(kMmThreads), 0, st, (const uint4*)bank,
-                       (const uint4*)query, n, d, nq, scores);
+void mfma_grid(int64_t rows, int* blocks, int64_t* rows_per_block) {
+    int64_t g = (rows + kMmRows - 1) / kMmRows;
+    const int64_t cap = compute_units() < kMmMaxBlocks ? compute_units() : kMmMaxBlocks;
+    if (g > cap) g = cap;
+    if (g < 1) g = 1;
+    int64_t rpb = (rows + g - 1) / g;
+    rpb = (rpb + 31) / 32 * 32;
+    *blocks = (int)g;
+    *rows_per_block = rpb;
+}
+
+int mfma_max_blocks() { return kMmMaxBlocks; }
+
+hipError_t launch_scan_mfma(const void* query, const void* bank, int d, int nq, int64_t row_begin,
+                            int64_t row_end, float* scores, int64_t ld, hipStream_t st) {
+    int G;
+    int64_t rpb;
+    mfma_grid(row_end - row_begin, &G, &rpb);
+    dim3 grid((unsigned)G, (unsigned)((nq + kMmQ - 1) / kMmQ));
+    hipLaunchKernelGGL(scan_mfma_kernel<false>, grid, dim3(kMmThreads), 0, st, (const uint4*)bank,
+                       (const uint4*)query, d, nq, row_begin, row_end, rpb, scores, ld,
+                       (const uint64_t*)nullptr, 1, (uint64_t*)nullptr, (uint32_t*)nullptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan_mfma_filter(const void* query, const void* bank, int d, int nq,
+                                   int64_t row_begin, int64_t row_end, const uint64_t* tau_keys,
+                                   int k, uint64_t* regions, uint32_t* counts, hipStream_t st) {
+    int G;
+    int64_t rpb;
+    mfma_grid(row_end - row_begin, &G, &rpb);
+    dim3 grid((unsigned)G, (unsigned)((nq + kMmQ - 1) / kMmQ));
+    hipLaunchKernelGGL(scan_mfma_kernel<true>, grid, dim3(kMmThreads), 0, st, (const uint4*)bank,
+                       (const uint4*)query, d, nq, row_begin, row_end, rpb, (float*)nullptr,
+                       (int64_t)0, tau_keys, k, regions, counts);
     return hipGetLastError();
 }
 
@@ -350,8 +510,10 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// One block selects the `want` largest keys of a chunk of up to
-// kSelThreads * kSelKpt inputs (keys are distinct: the low word is ~id).
+// One block selects the `want` = min(k, valid keys) largest keys held in its
+// registers (kSelKpt per thread; keys are distinct: the low word is ~id, and
+// 0 marks an empty entry). On return sh.sel[0 .. want) holds them, best
+// first, and every thread has passed a barrier after they were written.
 //  1. Lower bound: thread t folds its keys' maximum into group t mod want;
 //     the smallest group maximum tau has at least `want` keys >= it (one per
 //     group), so the answer lies among the keys >= tau, typically a few
@@ -360,35 +522,9 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 //     few, ranked exactly by pairwise comparison, which also orders them;
 //     otherwise a radix select over the candidates picks the `want` largest
 //     (8-bit digits from the highest differing bit) and those are ranked.
-// FROM_SCORES: inputs are fp32 scores [nq][M] and a key's id is its index;
-// otherwise inputs are keys [nq][M] where 0 marks an empty entry.
-template <bool FROM_SCORES>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores,
-                                                             const uint64_t* __restrict__ keys_in,
-                                                             int64_t M, int k, int nchunks,
-                                                             uint64_t* __restrict__ cand_out,
-                                                             int32_t* __restrict__ out_ids,
-                                                             float* __restrict__ out_scores) {
-    __shared__ SelShared sh;
+__device__ int select_block(const uint64_t (&key)[kSelKpt], int k, SelShared& sh) {
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    const int q = blockIdx.y;
-    const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
-
-    uint64_t key[kSelKpt];
-#pragma unroll
-    for (int i = 0; i < kSelKpt; ++i) {
-        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
-        uint64_t kv = 0;
-        if (idx < M) {
-            if (FROM_SCORES)
-                kv = rank_key(scores[(int64_t)q * M + idx], (uint32_t)idx);
-            else
-                kv = keys_in[(int64_t)q * M + idx];
-        }
-        key[i] = kv;  // nonzero iff valid: ~id has its top bit set for ids < 2^31
-    }
-
     // ---- valid count (wave ballots) ----
     uint32_t wc = 0;
 #pragma unroll
@@ -399,7 +535,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     uint32_t valid_total = 0;
 #pragma unroll
     for (int w = 0; w < kSelWaves; ++w) valid_total += sh.wcnt[w];
-    const int want = (int)min<int64_t>(k, valid_total);
+    const int want = (int)min_i64(k, valid_total);
 
     // ---- 1. lower bound tau ----
     uint64_t tau = 1;  // every valid key is >= 1
@@ -543,6 +679,41 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
         __syncthreads();
     }
 
+    return want;
+}
+
+// Top-k of one chunk of up to kSelThreads * kSelKpt inputs per block.
+// FROM_SCORES: inputs are fp32 scores [nq][M] and a key's id is its index;
+// otherwise inputs are keys [nq][M] where 0 marks an empty entry. With
+// out_ids the block writes the final ranking, else its `k` winners (0-padded)
+// to cand_out[q][chunk][k].
+template <bool FROM_SCORES>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores,
+                                                             const uint64_t* __restrict__ keys_in,
+                                                             int64_t M, int k, int nchunks,
+                                                             uint64_t* __restrict__ cand_out,
+                                                             int32_t* __restrict__ out_ids,
+                                                             float* __restrict__ out_scores) {
+    __shared__ SelShared sh;
+    const int t = threadIdx.x;
+    const int q = blockIdx.y;
+    const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
+
+    uint64_t key[kSelKpt];
+#pragma unroll
+    for (int i = 0; i < kSelKpt; ++i) {
+        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
+        uint64_t kv = 0;
+        if (idx < M) {
+            if (FROM_SCORES)
+                kv = rank_key(scores[(int64_t)q * M + idx], (uint32_t)idx);
+            else
+                kv = keys_in[(int64_t)q * M + idx];
+        }
+        key[i] = kv;  // nonzero iff valid: ~id has its top bit set for ids < 2^31
+    }
+    const int want = select_block(key, k, sh);
+
     // ---- output, best first ----
     if (out_ids) {
         for (int i = t; i < want; i += kSelThreads) {
@@ -553,6 +724,81 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     } else {
         uint64_t* dst = cand_out + ((int64_t)q * nchunks + blockIdx.x) * k;
         for (int i = t; i < k; i += kSelThreads) dst[i] = i < want ? sh.sel[i] : 0ull;
+    }
+}
+
+// Final ranking of the filtered matrix-core scan, one block per query. The
+// candidates of query q are the k keys of the sample, `first[q][0 .. k)`,
+// then the survivors of every scan block g, regions[q][g][0 .. counts[q][g]).
+// They are taken in chunks: the first chunk holds the first
+// kSelThreads * kSelKpt candidates; every later chunk holds the winners so
+// far and the next candidates, so any number of survivors is ranked exactly.
+__global__ __launch_bounds__(kSelThreads) void select_regions_kernel(
+    const uint64_t* __restrict__ first, const uint64_t* __restrict__ regions,
+    const uint32_t* __restrict__ counts, int G, int64_t rcap, int k,
+    int32_t* __restrict__ out_ids, float* __restrict__ out_scores) {
+    __shared__ SelShared sh;
+    __shared__ int64_t s_pre[kSelThreads + 1];   // survivors before region g
+    __shared__ int64_t s_wave_tot[kSelWaves];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int q = blockIdx.x;
+    const uint64_t* fq = first + (int64_t)q * k;
+    const uint64_t* rq = regions + (int64_t)q * G * rcap;
+
+    // exclusive prefix of the region counts (G <= kSelThreads)
+    const int64_t c = t < G ? (int64_t)counts[(int64_t)q * G + t] : 0;
+    const int64_t incl = wave_incl_scan(c, lane);
+    if (lane == 63) s_wave_tot[wave] = incl;
+    __syncthreads();
+    int64_t excl = incl - c;
+    for (int w = 0; w < wave; ++w) excl += s_wave_tot[w];
+    if (t < G) s_pre[t] = excl;
+    if (t == G - 1) s_pre[G] = excl + c;  // all survivors
+    __syncthreads();
+    const int64_t total = (int64_t)k + s_pre[G];
+
+    constexpr int64_t kChunk = (int64_t)kSelThreads * kSelKpt;
+    int64_t next = 0;   // candidates consumed so far
+    int carried = 0;    // winners carried into this chunk (slots 0 .. carried)
+    uint64_t carry = 0;
+    int want;
+    while (true) {
+        uint64_t key[kSelKpt];
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            const int64_t slot = t + (int64_t)i * kSelThreads;
+            uint64_t kv = 0;
+            if (slot < carried) {
+                kv = carry;  // only i == 0 and t < carried
+            } else {
+                const int64_t x = next + slot - carried;
+                if (x < total) {
+                    if (x < k) {
+                        kv = fq[x];
+                    } else {
+                        const int64_t y = x - k;
+                        int lo = 0, hi = G - 1;  // last region g with s_pre[g] <= y
+                        while (lo < hi) {
+                            const int mid = (lo + hi + 1) >> 1;
+                            if (s_pre[mid] <= y) lo = mid; else hi = mid - 1;
+                        }
+                        kv = rq[(int64_t)lo * rcap + (y - s_pre[lo])];
+                    }
+                }
+            }
+            key[i] = kv;
+        }
+        next += kChunk - carried;
+        want = select_block(key, k, sh);
+        if (next >= total) break;
+        carried = want;
+        carry = t < want ? sh.sel[t] : 0ull;
+        __syncthreads();  // sel is rewritten by the next chunk
+    }
+    for (int i = t; i < want; i += kSelThreads) {
+        const uint64_t me = sh.sel[i];
+        out_ids[(int64_t)q * k + i] = (int32_t)key_id(me);
+        if (out_scores) out_scores[(int64_t)q * k + i] = key_score(me);
     }
 }
 
@@ -572,6 +818,15 @@ hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, in
     dim3 grid((unsigned)nchunks, (unsigned)nq);
     hipLaunchKernelGGL((select_kernel<false>), grid, dim3(kSelThreads), 0, st,
                        (const float*)nullptr, keys, M, k, nchunks, cand, out_ids, out_scores);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_regions(const uint64_t* first, const uint64_t* regions,
+                                 const uint32_t* counts, int G, int64_t rcap, int k, int nq,
+                                 int32_t* out_ids, float* out_scores, hipStream_t st) {
+    if (G < 1 || G > kSelThreads) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(select_regions_kernel, dim3((unsigned)nq), dim3(kSelThreads), 0, st, first,
+                       regions, counts, G, rcap, k, out_ids, out_scores);
     return hipGetLastError();
 }
 

@@ -90,6 +90,58 @@ def test_retrieve_exact_ties_matrix_core_path():
     assert len(set(buf.scores[5, :4].tolist())) == 1
 
 
+def _ranked_against_oracle(q, bank, k):
+    nq, d = q.shape
+    n = bank.shape[0]
+    buf = RequestBuffers(n=n, d=d, k=k, nq=nq, emb_dtype=bank.dtype, max_tokens=1)
+    buf.retrieve(q, bank)
+    torch.cuda.synchronize()
+    gids, gsc = buf.ids.cpu().numpy(), buf.scores.cpu().numpy()
+    qh, odt = host_emb(q)
+    bh, _ = host_emb(bank)
+    ids_o, _, s_all = oracle.retrieve(qh, bh, n, d, k, nq, 0, odt)
+    near = 0
+    for r in range(nq):
+        near += parity.check_ids(gids[r], ids_o[r], s_all[r], n)
+        rows = oracle.bf16_to_f64(bh[gids[r]])
+        qd = oracle.bf16_to_f64(qh[r])
+        parity.check_scores(gsc[r], s_all[r][gids[r]], np.abs(rows * qd).sum(axis=1))
+    return gids, near
+
+
+def test_retrieve_filtered_scan_every_row_survives():
+    # matrix-core path with a row sample: the rows after the sample all equal
+    # query 0, so for it every one of them scores at or above the sample's
+    # k-th best. Every survivor region fills to capacity and the final ranking
+    # runs over several chunks; exact ties go to the lower ids.
+    g = torch.Generator(device="cuda").manual_seed(91)
+    n, d, k, nq, S = 100_000, 64, 50, 32, 16384
+    bank = torch.randn(n, d, generator=g, device="cuda")
+    bank = (bank / bank.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    v = bank[7].clone()
+    bank[S:] = v
+    q = (torch.randn(nq, d, generator=g, device="cuda"))
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    q[0] = v
+    gids, near = _ranked_against_oracle(q, bank, k)
+    assert gids[0][0] == 7 and list(gids[0][1:]) == list(range(S, S + k - 1))
+    log(f"filtered scan, all rows survive for one query: near-tie swaps {near}")
+
+
+def test_retrieve_filtered_scan_negative_scores():
+    # every score is negative, so the sample threshold is below the zero
+    # scores of the padding rows of partial tiles: they must not be ranked
+    g = torch.Generator(device="cuda").manual_seed(92)
+    n, d, k, nq = 40_000, 128, 20, 40
+    bank = torch.rand(n, d, generator=g, device="cuda") + 0.01
+    bank = (bank / bank.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    q = -(torch.rand(nq, d, generator=g, device="cuda") + 0.01)
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    gids, near = _ranked_against_oracle(q, bank, k)
+    assert (gids >= 0).all() and (gids < n).all()
+    log(f"filtered scan, negative scores: near-tie swaps {near}")
+
+
 def test_retrieve_signed_zero_scores_tie():
     # every score is +0 or -0: they are equal, so ranks follow the ids
     n, d = 500, 16
