@@ -53,14 +53,20 @@ __device__ __forceinline__ float wave_multi_sum(float (&a)[V], int lane, int* wh
     int idx = 0;
 #pragma unroll
     for (int half = V / 2, off = 32; half >= 1; half >>= 1, off >>= 1) {
-        const bool upper = (lane & off) != 0;
+        // the upper lane of each pair keeps the high half of the values; the
+        // choice is a bit blend of two statically indexed registers (a
+        // conditional pick between array elements is turned by the compiler
+        // into a dynamically indexed read, i.e. a compare/select chain over
+        // the whole array)
+        const uint32_t m = 0u - (uint32_t)((lane & off) != 0);
 #pragma unroll
         for (int i = 0; i < half; ++i) {
-            float keep = upper ? a[i + half] : a[i];
-            float send = upper ? a[i] : a[i + half];
+            const uint32_t lo = __float_as_uint(a[i]), hi = __float_as_uint(a[i + half]);
+            const float keep = __uint_as_float((hi & m) | (lo & ~m));
+            const float send = __uint_as_float((lo & m) | (hi & ~m));
             a[i] = keep + __shfl_xor(send, off, kWave);
         }
-        if (upper) idx += half;
+        idx += half & (int)m;
     }
     constexpr int kSteps = (V >= 64) ? 0 : 6 - __builtin_ctz(V);
     float v = a[0];
@@ -176,16 +182,15 @@ hipError_t launch_scan(const void* query, const void* bank, int64_t n, int d, in
 // Scores for nq queries against one bank form the product bank (n x d) times
 // queries^T (d x nq). A persistent 512-thread block owns one contiguous,
 // equal share of the bank rows and walks it in tiles of 256 rows x 256
-// queries; its 4 waves (one per SIMD, so each may hold 512 registers) each
-// accumulate 128 rows x 128 queries with v_mfma_f32_32x32x16_bf16 (exact bf16
-// products, fp32 sums). The reduction
+// queries; each wave accumulates kMmWaveRows rows x 128 queries with
+// v_mfma_f32_32x32x16_bf16 (exact bf16 products, fp32 sums). The reduction
 // dimension advances in chunks of 64: each chunk of the bank tile (32 KiB)
 // and of the query tile (32 KiB) is staged in shared memory, double
 // buffered. The bank is the only operand that comes from HBM (the query
 // tile stays in L2), so every thread keeps kMmDepth bank chunks in flight
 // in registers, and the pipeline runs on across tile boundaries. Rows are
 // 128 bytes in shared memory and the eight 16-byte units of a row are
-// XOR-swizzled by (row & 7), so the 32 rows a fragment read touches fall in
+// XOR-swizzled (swz below), so the rows a fragment read touches fall in
 // distinct banks.
 //
 // Two epilogues per finished tile:
@@ -203,7 +208,10 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr int kMmRows = 256;     // bank rows per tile
 constexpr int kMmQ = 256;        // queries per tile
 constexpr int kMmK = 64;         // reduction chunk
-constexpr int kMmThreads = 256;  // 4 waves: 2 row groups x 2 query groups
+constexpr int kMmWaveRows = 64;                  // bank rows per wave (x 128 queries)
+constexpr int kMmFragA = kMmWaveRows / 32;        // 32-row fragments per wave
+constexpr int kMmRowGroups = kMmRows / kMmWaveRows;
+constexpr int kMmThreads = kMmRowGroups * 2 * 64;  // row groups x 2 query groups
 constexpr int kMmDepth = 2;      // chunks in flight per thread
 constexpr int kMmSlots = kMmRows * 8 / kMmThreads;  // 16-byte staging slots per thread
 constexpr int kMmMaxBlocks = 1024;
@@ -225,6 +233,12 @@ __device__ __forceinline__ uint4 buffer_load16(rsrc_t r, uint32_t off) {
 
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond any descriptor here (<= 4 MiB)
 
+// Shared-memory swizzle of the eight 16-byte units of a 128-byte row: any 8
+// consecutive rows, and the 8 even or 8 odd rows of any 16 consecutive rows,
+// put a given unit in distinct 16-byte bank groups, so fragment reads of 32
+// consecutive rows are conflict-free with 128- and 256-byte bank cycles.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
 template <bool FILTER>
 __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
     const uint4* __restrict__ bank, const uint4* __restrict__ query, int d, int nq,
@@ -235,7 +249,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
     __shared__ uint4 sB[2][kMmQ * 8];
     __shared__ uint32_t s_cnt[FILTER ? kMmQ : 1];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int wr = wave & 1, wq = wave >> 1;
+    const int wr = wave % kMmRowGroups, wq = wave / kMmRowGroups;
     const int q0 = blockIdx.y * kMmQ;
     const int G = gridDim.x;
     const int units = d >> 3;                 // 16-byte units per row
@@ -284,28 +298,29 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < kMmSlots; ++j) {
             const int r = r_t + kRowStep * j;
-            sA[buf][r * 8 + (u_t ^ (r & 7))] = a[j];
-            sB[buf][r * 8 + (u_t ^ (r & 7))] = b[j];
+            sA[buf][r * 8 + (u_t ^ swz(r))] = a[j];
+            sB[buf][r * 8 + (u_t ^ swz(r))] = b[j];
         }
     };
 
-    f32x16_t acc[4][4];
+    f32x16_t acc[kMmFragA][4];
 
-    // every fragment row / column this lane reads is = lane (mod 8), so one
+    // every fragment row / column this lane reads is = lane (mod 32), so one
     // swizzled unit offset per reduction step serves all of them
-    const uint4* pa = &sA[0][(wr * 128 + (lane & 31)) * 8];
+    const uint4* pa = &sA[0][(wr * kMmWaveRows + (lane & 31)) * 8];
     const uint4* pb = &sB[0][(wq * 128 + (lane & 31)) * 8];
     auto compute = [&](int buf) {
 #pragma unroll
         for (int ks = 0; ks < kMmK / 16; ++ks) {
-            const int off = buf * (kMmRows * 8) + ((ks * 2 + (lane >> 5)) ^ (lane & 7));
-            bf16x8_t fa[4], fb[4];
+            const int off = buf * (kMmRows * 8) + ((ks * 2 + (lane >> 5)) ^ swz(lane & 31));
+            bf16x8_t fa[kMmFragA], fb[4];
 #pragma unroll
-            for (int a = 0; a < 4; ++a) fa[a] = __builtin_bit_cast(bf16x8_t, pa[a * 32 * 8 + off]);
+            for (int a = 0; a < kMmFragA; ++a)
+                fa[a] = __builtin_bit_cast(bf16x8_t, pa[a * 32 * 8 + off]);
 #pragma unroll
             for (int b = 0; b < 4; ++b) fb[b] = __builtin_bit_cast(bf16x8_t, pb[b * 32 * 8 + off]);
 #pragma unroll
-            for (int a = 0; a < 4; ++a)
+            for (int a = 0; a < kMmFragA; ++a)
 #pragma unroll
                 for (int b = 0; b < 4; ++b)
                     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
@@ -325,7 +340,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
     auto epilogue = [&](int tile) {
         const int64_t r0 = blk0 + (int64_t)tile * kMmRows;
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < kMmFragA; ++a)
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
                 const int qq = wq * 128 + b * 32 + (lane & 31);
@@ -343,7 +358,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
                     if (!(mx < tau_s[b]) && q < nq) {
 #pragma unroll
                         for (int e = 0; e < 16; ++e) {
-                            const int rr = tile * kMmRows + wr * 128 + a * 32 + 8 * (e >> 2) +
+                            const int rr = tile * kMmRows + wr * kMmWaveRows + a * 32 + 8 * (e >> 2) +
                                            4 * (lane >> 5) + (e & 3);  // row within the share
                             if (!(v[e] < tau_s[b]) && rr < nrows) {
                                 // the region address is formed here only (the
@@ -366,7 +381,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
                     float* out = scores + (int64_t)q * ld - row_begin;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const int64_t row = r0 + wr * 128 + a * 32 + 8 * g + 4 * (lane >> 5);
+                        const int64_t row = r0 + wr * kMmWaveRows + a * 32 + 8 * g + 4 * (lane >> 5);
                         if (row + 3 < blk1 && ((ld | (row - row_begin)) & 3) == 0) {
                             *(float4*)(out + row) =
                                 make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
@@ -396,7 +411,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
     __syncthreads();
     for (int tile = 0; tile < ntiles; ++tile) {
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < kMmFragA; ++a)
 #pragma unroll
             for (int b = 0; b < 4; ++b) acc[a][b] = f32x16_t{};
         for (int kc0 = 0; kc0 < nk; kc0 += kMmDepth) {
@@ -406,6 +421,9 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
                 const int buf = s & 1;
                 load_b(s + kMmDepth, rb[p]);
                 load_a(s + kMmDepth, ra[p]);
+                // issue the loads before this step's matrix work (the
+                // scheduler would otherwise sink them below it)
+                __builtin_amdgcn_sched_barrier(0);
                 compute(buf);
                 if (s + 1 < steps)
                     store_chunk(buf ^ 1, ra[(p + 1) % kMmDepth], rb[(p + 1) % kMmDepth]);
