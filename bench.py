@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+PCIE_PEAK_GBPS = 64.0     # PCIe 5.0 x16, one direction
 HBM_PEAK_GBPS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
@@ -51,6 +52,11 @@ def parse():
     ap.add_argument("--detail", action="store_true",
                     help="also time one stream (latency) and each call separately")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
+    ap.add_argument("--store", default="device", choices=["device", "host"],
+                    help="where the pre-RoPE K/V store lives: HBM, or pinned host memory "
+                         "that the inject kernel reads over PCIe")
+    ap.add_argument("--payloads", type=int, default=2048,
+                    help="distinct fact payloads of a host store (facts alias onto them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -75,6 +81,9 @@ def main():
          "retrieval1m": workloads.RETRIEVAL1M}[args.workload]
     if args.k is not None:
         w = w.with_(k=args.k)
+    host_store = args.store == "host"
+    if host_store and w.payloads is None:
+        w = w.with_(payloads=args.payloads)
     nsteps = args.warmup + args.steps
     # requests per slot-map/inject call: the whole batch, except the 1M-fact
     # case whose 256 requests' pages would not fit at once
@@ -83,7 +92,7 @@ def main():
 
     t0 = time.time()
     bank = workloads.make_bank(w, dev)
-    store = workloads.make_store(w, dev)
+    store = workloads.make_store(w, dev, host=host_store)
     queries = torch.stack([workloads.make_queries(w, dev, variant=i) for i in range(nsteps)])
     region_bytes = 2 * int(1.1 * wave * w.max_blocks) * w.page_size * w.L * w.H * w.D * 2
     R = max(1, min(8, int(60e9 // region_bytes)))
@@ -272,7 +281,7 @@ def main():
 
     # ---- CPU baseline: the oracle on the host for a bounded sample ------------
     cpu = None
-    if not args.no_cpu_baseline and args.workload == "llama8b":
+    if not args.no_cpu_baseline and args.workload == "llama8b" and not host_store:
         cpu = cpu_baseline(w, bank, store, queries, bts, args, torch)
 
     out = {
@@ -297,6 +306,9 @@ def main():
                          f"start_pos {w.start_pos}"),
             "k": w.k, "n": w.n, "nq": w.nq, "kv_dtype": "bf16", "emb_dtype": w.emb_dtype,
             "mean_m_tokens_per_step": round(statistics.fmean(m_steps), 1),
+            "store": ("pinned host memory, read over PCIe "
+                      f"({w.payloads} payloads, {2 * store['preK'].numel() * 2 / 1e9:.1f} GB)"
+                      if host_store else "HBM"),
         },
         "streams": S,
         "inject_launch_us": round(inj_launch_ms * 1e3, 2),
@@ -320,6 +332,16 @@ def main():
             "traffic": measured_traffic() if args.workload == "llama8b" and w.k == 50 else None,
             "traffic_unit": "HBM bytes per launch (scaled FETCH_SIZE + WRITE_SIZE)",
             "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves),
+        } if not host_store else {
+            # the store half of the inject traffic crosses the host link
+            "bound": "pcie",
+            "kernel": "inject_kernel",
+            "achieved": round(achieved / 2, 1),
+            "peak": PCIE_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / 2 / PCIE_PEAK_GBPS, 4),
+            "traffic": None,
+            "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves / 2),
         },
         "cpu_baseline": cpu,
     }

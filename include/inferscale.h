@@ -167,7 +167,12 @@ int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
  * j < D/2. The angle is formed and reduced in fp64, its sine and cosine are
  * fp32, the rotation is fp32 and each output is rounded to nearest-even bf16.
  *
- *   preK, V        bf16 [L][T_store][H][D] device, 16-byte aligned
+ *   preK, V        bf16 [L][T_store][H][D], 16-byte aligned: device memory of
+ *                  the current device, or pinned host memory mapped into its
+ *                  address space at the same address (hipHostMalloc), which
+ *                  the kernel then reads over the host link -- the CPU-resident
+ *                  KV store of §6.8 and App. C. Any other pointer is rejected
+ *                  with IS_ERR_INVALID before anything is enqueued.
  *   slots, positions  [nq][max_tokens] as written by is_slot_map
  *   paged_k, paged_v  bf16 [L][num_slots][H][D] device, 16-byte aligned
  *   fact_offsets   per-request [n] int64 row offsets into the store

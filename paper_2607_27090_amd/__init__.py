@@ -77,6 +77,19 @@ def load_library() -> ctypes.CDLL:
     return lib
 
 
+def _store_ptr(x):
+    """Pointer of a pre-RoPE store tensor: device memory, or pinned host memory
+    that the inject kernel reads over the host link (the library checks that
+    it is mapped for the device)."""
+    if isinstance(x, torch.Tensor) and not x.is_cuda:
+        if not x.is_pinned():
+            raise ValueError("a host-resident store must be pinned (pin_memory=True)")
+        if not x.is_contiguous():
+            raise ValueError("libinferscale takes contiguous tensors")
+        return x.data_ptr()
+    return _ptr(x)
+
+
 def _check(fn: str, rc: int) -> None:
     if rc != IS_OK:
         msg = load_library().is_last_error().decode(errors="replace")
@@ -154,7 +167,7 @@ def is_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *, f
               T_store, num_slots, status=None, stream=None) -> None:
     """Fused gather + RoPE + scatter (see include/inferscale.h)."""
     _check("is_inject", load_library().is_inject(
-        _ptr(ids), _ptr(preK), _ptr(V), _ptr(slots), _ptr(positions), float(rope_theta),
+        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(slots), _ptr(positions), float(rope_theta),
         _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens), _ptr(m), k, nq, n,
         lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots, _ptr(status),
         _stream(stream)))

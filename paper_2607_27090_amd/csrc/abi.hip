@@ -85,6 +85,39 @@ bool fused_applies(int64_t n, int32_t d, int32_t nq, int64_t bank_stride, int32_
     return is::scan_mfma_applies(n, d, nq, bank_stride, dtype) && n > 2 * is::select_chunk_len();
 }
 
+// A pre-RoPE store pointer is usable by the inject kernel if it is memory of
+// the current device, managed memory, or pinned host memory mapped into the
+// device's address space at the same address.
+int check_store_pointer(const void* p, const char* what) {
+    hipPointerAttribute_t a{};
+    const hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // do not leave the failure for the launch check
+        return fail(IS_ERR_INVALID, "%s is neither device memory nor mapped pinned host memory",
+                    what);
+    }
+    int dev = -1;
+    (void)hipGetDevice(&dev);
+    switch (a.type) {
+        case hipMemoryTypeDevice:
+            if (a.device != dev)
+                return fail(IS_ERR_INVALID, "%s is memory of device %d, not of the current device %d",
+                            what, a.device, dev);
+            return IS_OK;
+        case hipMemoryTypeManaged:
+            return IS_OK;
+        case hipMemoryTypeHost:
+            if (a.devicePointer != p)
+                return fail(IS_ERR_INVALID,
+                            "%s is pinned host memory not mapped at the same device address; pass "
+                            "the address hipHostGetDevicePointer returns", what);
+            return IS_OK;
+        default:
+            return fail(IS_ERR_INVALID, "%s is neither device memory nor mapped pinned host memory",
+                        what);
+    }
+}
+
 int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dtype) {
     if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
     if (d < 8 || d > 8192 || d % 8) return fail(IS_ERR_INVALID, "d=%d must be a multiple of 8 in [8, 8192]", d);
@@ -270,6 +303,12 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
         !aligned(positions, 4) || !aligned(fact_lens, 4) || !aligned(m, 4) ||
         (status && !aligned(status, 4)))
         return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    // the store may be device memory or device-mapped pinned host memory
+    // (read over the host link); anything else would fault the kernel
+    int rc = check_store_pointer(preK, "preK");
+    if (rc) return rc;
+    rc = check_store_pointer(V, "V");
+    if (rc) return rc;
     hipError_t e = is::launch_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v,
                                      fact_offsets, fact_lens, m, k, nq, n, lens_stride,
                                      reverse_rank, max_tokens, L, H, D, T_store, num_slots, status,

@@ -163,11 +163,14 @@ def make_queries(w: Workload, device, variant: int = 0) -> torch.Tensor:
     return _to_emb(x, w)
 
 
-def make_store(w: Workload, device, chunk_tokens: int = 1 << 14):
+def make_store(w: Workload, device, chunk_tokens: int = 1 << 14, host: bool = False):
     """Pre-RoPE K and V stores plus per-fact lengths and row offsets.
 
     Returns dict(preK, V: bf16 [L][T_store][H][D]; fact_lens: int32 [banks][n];
-    fact_offsets: int64 [banks][n]; T_store)."""
+    fact_offsets: int64 [banks][n]; T_store). With host=True, preK and V live
+    in pinned host memory (the values are generated on `device` exactly as for
+    a device store and copied over chunk by chunk); lengths and offsets stay
+    on `device`."""
     banks = 1 if w.shared_bank else w.nq
     g = _gen(_seed(w, 3), "cpu")
     if w.payloads is None:
@@ -182,8 +185,9 @@ def make_store(w: Workload, device, chunk_tokens: int = 1 << 14):
         offs = poff[which]
         T_store = int(plen.sum())
     row = w.H * w.D
-    preK = torch.empty(w.L, T_store, row, dtype=torch.bfloat16, device=device)
-    V = torch.empty(w.L, T_store, row, dtype=torch.bfloat16, device=device)
+    where = dict(device="cpu", pin_memory=True) if host else dict(device=device)
+    preK = torch.empty(w.L, T_store, row, dtype=torch.bfloat16, **where)
+    V = torch.empty(w.L, T_store, row, dtype=torch.bfloat16, **where)
     gk = _gen(_seed(w, 4), device)
     gv = _gen(_seed(w, 5), device)
     for l in range(w.L):
