@@ -11,7 +11,8 @@ Paper passages followed (InferScale):
   * placement: §5.2 "Position policy" (contiguous facts, cumulative offsets,
     most relevant fact adjacent to the query);
   * slots: §2.2 paged KV cache (fixed-size blocks through a block table);
-  * rotation: §2.4 and Theorem "Chunked RoPE Injection" (§5.1);
+  * rotation: §2.4 and Theorem "Chunked RoPE Injection" (§5.1); with the
+    model's own rotary table and pair layout, §3.3 and §6.1;
   * composition and scatter: §3.3 and §3.4.
 """
 from __future__ import annotations
@@ -77,6 +78,15 @@ def _load():
     lib.oracle_inject.argtypes = [P, P, P, P, P, f64, P, P, P, P, P, i32, i32, i64, i64, i32,
                                   i32, i32, i32, i32, i64, i64, P]
     lib.oracle_inject.restype = ctypes.c_int
+    lib.oracle_rope_table_f64.argtypes = [P, f64, P, i32, i32, P]
+    lib.oracle_rope_table_f64.restype = None
+    lib.oracle_rope_table_bf16.argtypes = [P, i64, P, i32, i32, P]
+    lib.oracle_rope_table_bf16.restype = None
+    lib.oracle_default_inv_freq.argtypes = [f64, i32, P]
+    lib.oracle_default_inv_freq.restype = None
+    lib.oracle_inject_rotary.argtypes = [P, P, P, P, P, f64, P, P, P, P, P, i32, i32, i64, i64,
+                                         i32, i32, i32, i32, i32, i64, i64, P, i32, P]
+    lib.oracle_inject_rotary.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -197,10 +207,40 @@ def rope_rows_bf16(rows, positions, theta, H, D):
     return out.reshape(-1, H * D)
 
 
+def default_inv_freq(theta, D):
+    """inv_freq[j] = theta^(-2j/D), j < D/2 (binary64)."""
+    lib = _load()
+    out = np.empty(D // 2, dtype=np.float64)
+    lib.oracle_default_inv_freq(float(theta), D, _ptr(out))
+    return out
+
+
+def rope_table_f64(x, p, inv_freq, D, interleaved=False):
+    """R_p x with a given frequency table and pair layout (binary64)."""
+    lib = _load()
+    xs = _c(x, np.float64)
+    f = _c(inv_freq, np.float64)
+    y = np.empty_like(xs)
+    lib.oracle_rope_table_f64(_ptr(xs), float(p), _ptr(f), D, int(bool(interleaved)), _ptr(y))
+    return y
+
+
+def rope_table_bf16(x_bits, p, inv_freq, D, interleaved=False):
+    """bf16 head vector in, bf16 out, with a given table and pair layout."""
+    lib = _load()
+    xs = _c(x_bits, np.uint16)
+    f = _c(inv_freq, np.float64)
+    y = np.empty_like(xs)
+    lib.oracle_rope_table_bf16(_ptr(xs), int(p), _ptr(f), D, int(bool(interleaved)), _ptr(y))
+    return y
+
+
 def inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, fact_offsets,
            fact_lens, m, k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D,
-           T_store, num_slots):
-    """Writes paged_k / paged_v (uint16 arrays, modified in place); returns status."""
+           T_store, num_slots, inv_freq=None, interleaved=False):
+    """Writes paged_k / paged_v (uint16 arrays, modified in place); returns status.
+    inv_freq [D/2] (None: rope_theta's default table) and interleaved select
+    the model's rotary table and pair layout."""
     lib = _load()
     ids_ = _c(ids, np.int32)
     pk = _c(preK, np.uint16)
@@ -213,10 +253,12 @@ def inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, fact_of
     for a in (paged_k, paged_v):
         assert a.dtype == np.uint16 and a.flags["C_CONTIGUOUS"]
     status = np.zeros((1,), dtype=np.uint32)
-    rc = lib.oracle_inject(_ptr(ids_), _ptr(pk), _ptr(vv), _ptr(sl), _ptr(po), float(rope_theta),
-                           _ptr(paged_k), _ptr(paged_v), _ptr(fo), _ptr(fl), _ptr(mm), k, nq, n,
-                           lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
-                           _ptr(status))
+    f = None if inv_freq is None else _c(inv_freq, np.float64)
+    rc = lib.oracle_inject_rotary(_ptr(ids_), _ptr(pk), _ptr(vv), _ptr(sl), _ptr(po),
+                                  float(rope_theta), _ptr(paged_k), _ptr(paged_v), _ptr(fo),
+                                  _ptr(fl), _ptr(mm), k, nq, n, lens_stride, reverse_rank,
+                                  max_tokens, L, H, D, T_store, num_slots, _ptr(f),
+                                  int(bool(interleaved)), _ptr(status))
     if rc != 0:
         raise ValueError(f"oracle_inject rejected its arguments (rc={rc})")
     return int(status[0])

@@ -245,6 +245,42 @@ void oracle_rope_f64(const double* x, double p, double theta, int32_t D, double*
     }
 }
 
+/* The same rotation with the model's own rotary table (§3.3: composition
+ * applies RoPE with the model's rotary tables; §6.1: the evaluated models
+ * differ in their RoPE parameterisation): pair j < D/2 is turned by the angle
+ * a = p * inv_freq[j]. The pair is (j, j + D/2) in the half-split layout
+ * (interleaved == 0) and (2j, 2j + 1) in the interleaved one. Binary64. */
+void oracle_rope_table_f64(const double* x, double p, const double* inv_freq, int32_t D,
+                           int32_t interleaved, double* y)
+{
+    int32_t half = D / 2;
+    for (int32_t j = 0; j < half; ++j) {
+        double a = p * inv_freq[j];
+        double c = cos(a), s = sin(a);
+        int32_t i0 = interleaved ? 2 * j : j;
+        int32_t i1 = interleaved ? 2 * j + 1 : j + half;
+        double x0 = x[i0], x1 = x[i1];
+        y[i0] = x0 * c - x1 * s;
+        y[i1] = x1 * c + x0 * s;
+    }
+}
+
+/* The default table of the rotation above: inv_freq[j] = theta^(-2j/D). */
+void oracle_default_inv_freq(double theta, int32_t D, double* inv_freq)
+{
+    for (int32_t j = 0; j < D / 2; ++j) inv_freq[j] = pow(theta, -2.0 * (double)j / (double)D);
+}
+
+void oracle_rope_table_bf16(const uint16_t* x, int64_t p, const double* inv_freq, int32_t D,
+                            int32_t interleaved, uint16_t* y)
+{
+    double xd[1024], yd[1024];
+    if (D < 2 || D > 1024 || D % 2) return;
+    for (int32_t e = 0; e < D; ++e) xd[e] = oracle_bf16_to_double(x[e]);
+    oracle_rope_table_f64(xd, (double)p, inv_freq, D, interleaved, yd);
+    for (int32_t e = 0; e < D; ++e) y[e] = oracle_double_to_bf16(yd[e]);
+}
+
 /* bf16 head vector in, bf16 head vector out: decode, rotate in binary64,
  * round each element to nearest-even bf16. */
 void oracle_rope_bf16(const uint16_t* x, int64_t p, double theta, int32_t D, uint16_t* y)
@@ -265,19 +301,27 @@ void oracle_rope_bf16(const uint16_t* x, int64_t p, double theta, int32_t D, uin
  *   paged_v[l][slots[idx]][h][:] = V[l][src][h][:]      (bit copy)
  * Layouts: preK, V are [L][T_store][H][D]; pages are [L][num_slots][H][D];
  * all bf16. Nothing else in the pages is written. */
-int oracle_inject(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
-                  const int64_t* slots, const int32_t* positions, double rope_theta,
-                  uint16_t* paged_k, uint16_t* paged_v,
-                  const int64_t* fact_offsets, const int32_t* fact_lens,
-                  const int32_t* m, int32_t k, int32_t nq, int64_t n,
-                  int64_t lens_stride, int32_t reverse_rank, int32_t max_tokens,
-                  int32_t L, int32_t H, int32_t D, int64_t T_store, int64_t num_slots,
-                  uint32_t* status)
+/* The same with the model's rotary table and pair layout: inv_freq [D/2]
+ * (NULL: the default table of rope_theta) and interleaved as in
+ * oracle_rope_table_f64. */
+int oracle_inject_rotary(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
+                         const int64_t* slots, const int32_t* positions, double rope_theta,
+                         uint16_t* paged_k, uint16_t* paged_v,
+                         const int64_t* fact_offsets, const int32_t* fact_lens,
+                         const int32_t* m, int32_t k, int32_t nq, int64_t n,
+                         int64_t lens_stride, int32_t reverse_rank, int32_t max_tokens,
+                         int32_t L, int32_t H, int32_t D, int64_t T_store, int64_t num_slots,
+                         const double* inv_freq, int32_t interleaved, uint32_t* status)
 {
     if (!ids || !preK || !V || !slots || !positions || !paged_k || !paged_v ||
         !fact_offsets || !fact_lens || !m)
         return -1;
     if (k < 1 || nq < 1 || L < 1 || H < 1 || D < 2 || D % 2 || D > 1024) return -1;
+    double freq[512];
+    if (inv_freq)
+        for (int32_t j = 0; j < D / 2; ++j) freq[j] = inv_freq[j];
+    else
+        oracle_default_inv_freq(rope_theta, D, freq);
     uint32_t flags = 0;
     int64_t row = (int64_t)H * D;
     for (int32_t r = 0; r < nq; ++r) {
@@ -308,7 +352,8 @@ int oracle_inject(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
                     uint16_t* kd = paged_k + ((int64_t)l * num_slots + slot) * row;
                     uint16_t* vd = paged_v + ((int64_t)l * num_slots + slot) * row;
                     for (int32_t h = 0; h < H; ++h)
-                        oracle_rope_bf16(ks + (int64_t)h * D, p, rope_theta, D, kd + (int64_t)h * D);
+                        oracle_rope_table_bf16(ks + (int64_t)h * D, p, freq, D, interleaved,
+                                               kd + (int64_t)h * D);
                     memcpy(vd, vs, (size_t)row * sizeof(uint16_t));
                 }
             }
@@ -317,4 +362,18 @@ int oracle_inject(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
     }
     if (status) *status |= flags;
     return 0;
+}
+
+int oracle_inject(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
+                  const int64_t* slots, const int32_t* positions, double rope_theta,
+                  uint16_t* paged_k, uint16_t* paged_v,
+                  const int64_t* fact_offsets, const int32_t* fact_lens,
+                  const int32_t* m, int32_t k, int32_t nq, int64_t n,
+                  int64_t lens_stride, int32_t reverse_rank, int32_t max_tokens,
+                  int32_t L, int32_t H, int32_t D, int64_t T_store, int64_t num_slots,
+                  uint32_t* status)
+{
+    return oracle_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v,
+                                fact_offsets, fact_lens, m, k, nq, n, lens_stride, reverse_rank,
+                                max_tokens, L, H, D, T_store, num_slots, NULL, 0, status);
 }

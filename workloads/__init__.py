@@ -87,6 +87,31 @@ RETRIEVAL1M = Workload("retrieval-1m", L=32, H=8, D=128, n=1000000, len_lo=16, l
 ALL = [TINY, LLAMA8B, CONCURRENCY, LLAMA70B, RETRIEVAL1M]
 
 
+def llama31_inv_freq(D: int, theta: float = 500000.0, factor: float = 8.0,
+                     low_freq_factor: float = 1.0, high_freq_factor: float = 4.0,
+                     original_context: int = 8192):
+    """A model's own rotary table: Llama 3.1's published RoPE frequency
+    scaling applied to theta^(-2j/D) (binary64, [D/2]). Wavelengths below
+    original_context / high_freq_factor keep their frequency, those above
+    original_context / low_freq_factor are divided by `factor`, and the band
+    in between interpolates linearly in original_context / wavelength."""
+    import numpy as np
+    base = theta ** (-np.arange(0, D, 2, dtype=np.float64) / D)
+    out = base.copy()
+    lo_wl = original_context / low_freq_factor
+    hi_wl = original_context / high_freq_factor
+    for j, f in enumerate(base):
+        wl = 2.0 * math.pi / f
+        if wl < hi_wl:
+            continue
+        if wl > lo_wl:
+            out[j] = f / factor
+        else:
+            smooth = (original_context / wl - low_freq_factor) / (high_freq_factor - low_freq_factor)
+            out[j] = (1.0 - smooth) * f / factor + smooth * f
+    return out
+
+
 def kv_bytes_per_token(w: Workload) -> int:
     """Stored KV bytes of one fact token across all layers (K and V, bf16):
     2 * L * H * D * 2 (§3.5 with c = 1, b = 2)."""
