@@ -57,6 +57,10 @@ def parse():
                          "that the inject kernel reads over PCIe")
     ap.add_argument("--payloads", type=int, default=2048,
                     help="distinct fact payloads of a host store (facts alias onto them)")
+    ap.add_argument("--rope", default="default", choices=["default", "llama3.1", "interleaved"],
+                    help="rotary table / pair layout of the inject: theta^(-2j/D) half-split "
+                         "(is_inject), Llama 3.1's scaled table, or interleaved pairs "
+                         "(is_inject_rotary)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -71,7 +75,8 @@ def main():
 
     import torch
     import workloads
-    from paper_2607_27090_amd import is_inject, is_slot_map
+    from paper_2607_27090_amd import (IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED, is_inject,
+                                      is_inject_rotary, is_slot_map)
     from paper_2607_27090_amd.pipeline import RequestBuffers
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -121,15 +126,26 @@ def main():
                     lens_stride=lens_stride, max_blocks=bts.shape[-1], max_tokens=w.max_tokens,
                     status=b.status)
 
+    rope_table = None
+    if args.rope == "llama3.1":
+        rope_table = torch.from_numpy(workloads.llama31_inv_freq(w.D, w.theta)).to(dev)
+
     def inject(j, b=None):
         b = buf if b is None else b
         sl = slice(j * wave, (j + 1) * wave)
         ls = lens if lens_stride == 0 else lens[sl]
         os_ = offs if lens_stride == 0 else offs[sl]
-        is_inject(b.ids[sl], store["preK"], store["V"], b.slots[sl], b.positions[sl],
-                  w.theta, pk, pv, fact_offsets=os_, fact_lens=ls, m=b.m[sl], k=w.k, nq=wave,
-                  n=w.n, lens_stride=lens_stride, max_tokens=w.max_tokens, L=L, H=H, D=D,
+        kw = dict(fact_offsets=os_, fact_lens=ls, m=b.m[sl], k=w.k, nq=wave, n=w.n,
+                  lens_stride=lens_stride, max_tokens=w.max_tokens, L=L, H=H, D=D,
                   T_store=T, num_slots=num_slots, status=b.status)
+        if args.rope == "default":
+            is_inject(b.ids[sl], store["preK"], store["V"], b.slots[sl], b.positions[sl],
+                      w.theta, pk, pv, **kw)
+        else:
+            is_inject_rotary(b.ids[sl], store["preK"], store["V"], b.slots[sl], b.positions[sl],
+                             w.theta, pk, pv, inv_freq=rope_table,
+                             pairing=(IS_ROPE_INTERLEAVED if args.rope == "interleaved"
+                                      else IS_ROPE_HALF_SPLIT), **kw)
 
     def step(i, b=None):
         b = buf if b is None else b
@@ -306,6 +322,9 @@ def main():
                          f"start_pos {w.start_pos}"),
             "k": w.k, "n": w.n, "nq": w.nq, "kv_dtype": "bf16", "emb_dtype": w.emb_dtype,
             "mean_m_tokens_per_step": round(statistics.fmean(m_steps), 1),
+            "rope": {"default": f"theta^(-2j/D), pairs (j, j+D/2)",
+                     "llama3.1": "Llama 3.1 scaled table, pairs (j, j+D/2)",
+                     "interleaved": "theta^(-2j/D), pairs (2j, 2j+1)"}[args.rope],
             "store": ("pinned host memory, read over PCIe "
                       f"({w.payloads} payloads, {2 * store['preK'].numel() * 2 / 1e9:.1f} GB)"
                       if host_store else "HBM"),

@@ -189,6 +189,34 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
               int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
               int64_t num_slots, uint32_t* status, void* stream);
 
+/* pair layouts of is_inject_rotary */
+#define IS_ROPE_HALF_SPLIT 0  /* pairs (j, j + D/2): the rotate-half form (Llama, Mistral, Qwen) */
+#define IS_ROPE_INTERLEAVED 1 /* pairs (2j, 2j + 1) */
+
+/*
+ * is_inject_rotary -- is_inject with the model's own rotary table and pair
+ * layout (§3.3: composition applies RoPE with the model's rotary tables;
+ * §6.1: the evaluated models differ in their RoPE parameterisation, e.g.
+ * Llama 3.1's frequency scaling).
+ *
+ * Every argument of is_inject keeps its meaning, and:
+ *   inv_freq  binary64 [D/2] device array, the angular frequency of pair j
+ *             (radians per position): pair j of a token at position p turns
+ *             by p * inv_freq[j]. NULL: rope_theta^(-2j/D), exactly as
+ *             is_inject (rope_theta is then required to be positive and
+ *             finite; with a table it is ignored). 8-byte aligned. Entries
+ *             are not checked: a non-finite frequency gives non-finite keys.
+ *   pairing   IS_ROPE_HALF_SPLIT or IS_ROPE_INTERLEAVED.
+ * is_inject(...) is is_inject_rotary(..., NULL, IS_ROPE_HALF_SPLIT).
+ */
+int is_inject_rotary(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+                     const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+                     const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+                     int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+                     int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+                     int64_t num_slots, const double* inv_freq, int32_t pairing, uint32_t* status,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -36,8 +36,11 @@ IS_DEV_SRC_RANGE = 64
 IS_MAX_K = 1024
 IS_MAX_HEAD_DIM = 512
 
+IS_ROPE_HALF_SPLIT = 0
+IS_ROPE_INTERLEAVED = 1
+
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_slot_map", "is_inject")
+            "is_slot_map", "is_inject", "is_inject_rotary")
 
 
 class InferScaleError(RuntimeError):
@@ -73,6 +76,9 @@ def load_library() -> ctypes.CDLL:
     lib.is_inject.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32, i32,
                               i32, i32, i32, i64, i64, P, P]
     lib.is_inject.restype = ctypes.c_int
+    lib.is_inject_rotary.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32,
+                                     i32, i32, i32, i32, i64, i64, P, i32, P, P]
+    lib.is_inject_rotary.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -171,3 +177,18 @@ def is_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *, f
         _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens), _ptr(m), k, nq, n,
         lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots, _ptr(status),
         _stream(stream)))
+
+
+def is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *,
+                     fact_offsets, fact_lens, m, k, nq, n, lens_stride, reverse_rank=1,
+                     max_tokens, L, H, D, T_store, num_slots, inv_freq=None,
+                     pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
+    """is_inject with the model's rotary table (float64 device tensor [D/2],
+    None: rope_theta's default table) and pair layout (see include/inferscale.h)."""
+    if inv_freq is not None and inv_freq.dtype != torch.float64:
+        raise ValueError("inv_freq must be a float64 tensor")
+    _check("is_inject_rotary", load_library().is_inject_rotary(
+        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(slots), _ptr(positions),
+        float(rope_theta), _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens),
+        _ptr(m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+        _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))

@@ -276,15 +276,16 @@ int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
     return ok();
 }
 
-int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
-              const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
-              const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
-              int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
-              int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
-              int64_t num_slots, uint32_t* status, void* stream) {
+int is_inject_rotary(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+                     const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+                     const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+                     int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+                     int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+                     int64_t num_slots, const double* inv_freq, int32_t pairing, uint32_t* status,
+                     void* stream) {
     if (!ids || !preK || !V || !slots || !positions || !paged_k || !paged_v || !fact_offsets ||
         !fact_lens || !m)
-        return fail(IS_ERR_INVALID, "every array argument except status must be non-NULL");
+        return fail(IS_ERR_INVALID, "every array argument except status and inv_freq must be non-NULL");
     if (k < 1 || k > IS_MAX_K) return fail(IS_ERR_INVALID, "k=%d must be in [1, %d]", k, IS_MAX_K);
     if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
     if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
@@ -295,13 +296,16 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
     if ((int64_t)H * D > (1 << 20)) return fail(IS_ERR_UNSUPPORTED, "H*D=%lld too large", (long long)H * D);
     if (T_store < 0 || num_slots < 0 || max_tokens < 0 || lens_stride < 0)
         return fail(IS_ERR_INVALID, "T_store, num_slots, max_tokens and lens_stride must be >= 0");
-    if (!(rope_theta > 0.f) || !std::isfinite(rope_theta))
+    if (!inv_freq && (!(rope_theta > 0.f) || !std::isfinite(rope_theta)))
         return fail(IS_ERR_INVALID, "rope_theta must be positive and finite");
+    if (pairing != IS_ROPE_HALF_SPLIT && pairing != IS_ROPE_INTERLEAVED)
+        return fail(IS_ERR_INVALID, "pairing=%d is neither IS_ROPE_HALF_SPLIT nor IS_ROPE_INTERLEAVED",
+                    pairing);
     if (!aligned(preK, 16) || !aligned(V, 16) || !aligned(paged_k, 16) || !aligned(paged_v, 16))
         return fail(IS_ERR_INVALID, "preK, V, paged_k and paged_v must be 16-byte aligned");
     if (!aligned(slots, 8) || !aligned(fact_offsets, 8) || !aligned(ids, 4) ||
         !aligned(positions, 4) || !aligned(fact_lens, 4) || !aligned(m, 4) ||
-        (status && !aligned(status, 4)))
+        (status && !aligned(status, 4)) || (inv_freq && !aligned(inv_freq, 8)))
         return fail(IS_ERR_INVALID, "misaligned pointer argument");
     // the store may be device memory or device-mapped pinned host memory
     // (read over the host link); anything else would fault the kernel
@@ -311,10 +315,22 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
     if (rc) return rc;
     hipError_t e = is::launch_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v,
                                      fact_offsets, fact_lens, m, k, nq, n, lens_stride,
-                                     reverse_rank, max_tokens, L, H, D, T_store, num_slots, status,
-                                     (hipStream_t)stream);
+                                     reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+                                     inv_freq, pairing, status, (hipStream_t)stream);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "inject launch: %s", hipGetErrorString(e));
     return ok();
+}
+
+int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
+              const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
+              const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
+              int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+              int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+              int64_t num_slots, uint32_t* status, void* stream) {
+    return is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v,
+                            fact_offsets, fact_lens, m, k, nq, n, lens_stride, reverse_rank,
+                            max_tokens, L, H, D, T_store, num_slots, nullptr, IS_ROPE_HALF_SPLIT,
+                            status, stream);
 }
 
 }  // extern "C"

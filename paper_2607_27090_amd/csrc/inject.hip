@@ -2,13 +2,16 @@
 // composition: stored pre-RoPE keys are rotated on the fly to the positions
 // the request assigns; §3.4: the composed K and V go into the request's
 // blocks through the slot mapping; §2.4 / Theorem "Chunked RoPE Injection",
-// §5.1: R_p is the block-diagonal rotation by p * theta^(-2j/D)).
+// §5.1: R_p is the block-diagonal rotation by p * theta^(-2j/D), or by p
+// times the model's own rotary table, §3.3 and §6.1).
 //
 // Work decomposition (HBM-bound streaming copy with a little math):
 //   * a thread item is (placed token, 16-element lane unit of a head): it owns
 //     elements [8u, 8u+8) of the first half of head h and the matching
 //     elements [D/2 + 8u, D/2 + 8u + 8) of the second half, so every rotation
-//     pair (j, j + D/2) lives in one thread and all loads/stores are 16 bytes;
+//     pair lives in one thread in both pair layouts -- (j, j + D/2), the
+//     half-split one, and (2j, 2j + 1), the interleaved one -- and all
+//     loads/stores are 16 bytes;
 //     one wave covers one full (token, layer) row of H*D elements when
 //     H*D == 1024, i.e. 2 KiB of K and 2 KiB of V, read and written as whole
 //     128-byte lines;
@@ -52,14 +55,33 @@ __device__ __forceinline__ void rotate8(const uint4 lo, const uint4 hi, const fl
     out_hi = make_uint4(yb[0], yb[1], yb[2], yb[3]);
 }
 
-__global__ __launch_bounds__(kInjThreads) void inject_kernel(
+// Interleaved layout: every 32-bit word of lo / hi is one pair (2j, 2j + 1);
+// lo holds pairs with angles c[0..3] / s[0..3], hi those with c[4..7] / s[4..7].
+__device__ __forceinline__ void rotate8_interleaved(const uint4 lo, const uint4 hi,
+                                                    const float (&c)[8], const float (&s)[8],
+                                                    uint4& out_lo, uint4& out_hi) {
+    const uint32_t in[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    uint32_t out[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float x0 = bf16_lo(in[e]), x1 = bf16_hi(in[e]);
+        const float y0 = fmaf(x0, c[e], -(x1 * s[e]));
+        const float y1 = fmaf(x1, c[e], x0 * s[e]);
+        out[e] = pack_bf16x2(y0, y1);
+    }
+    out_lo = make_uint4(out[0], out[1], out[2], out[3]);
+    out_hi = make_uint4(out[4], out[5], out[6], out[7]);
+}
+
+template <bool INTERLEAVED>
+__global__ __launch_bounds__(kInjThreads, 4) void inject_kernel(
     const int32_t* __restrict__ ids, const uint4* __restrict__ preK, const uint4* __restrict__ V,
     const int64_t* __restrict__ slots, const int32_t* __restrict__ positions, float rope_theta,
     uint4* __restrict__ paged_k, uint4* __restrict__ paged_v,
     const int64_t* __restrict__ fact_offsets, const int32_t* __restrict__ fact_lens,
     const int32_t* __restrict__ m_dev, int32_t k, int64_t n, int64_t lens_stride,
     int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
-    int64_t num_slots, uint32_t* __restrict__ status) {
+    int64_t num_slots, const double* __restrict__ inv_freq, uint32_t* __restrict__ status) {
     __shared__ int64_t s_b[IS_MAX_K + 1];     // placed-token offset of each fact
     __shared__ int64_t s_off[IS_MAX_K];       // store row of each fact, -1: skip
     __shared__ double s_invf[IS_MAX_HEAD_DIM / 2];
@@ -144,7 +166,8 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
     const int64_t incl = wave_incl_scan(run, lane);
     if (lane == 63) s_wave_tot[wave] = incl;
     if (t < (D >> 1))
-        s_invf[t] = exp2(-(2.0 * (double)t / (double)D) * log2((double)rope_theta));
+        s_invf[t] = inv_freq ? inv_freq[t]
+                             : exp2(-(2.0 * (double)t / (double)D) * log2((double)rope_theta));
     __syncthreads();
     int64_t excl = incl - run;
     for (int w = 0; w < wave; ++w) excl += s_wave_tot[w];
@@ -238,7 +261,12 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
                 const double p = (double)pos_in;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const double a = p * s_invf[sub * 8 + e];
+                    // pair of angle e: half-split, j = 8 sub + e; interleaved,
+                    // the 4 pairs of each 16-byte half, j = 4 sub + e and
+                    // D/4 + 4 sub + e - 4
+                    const int j = INTERLEAVED ? (e < 4 ? 4 * sub + e : (D >> 2) + 4 * sub + e - 4)
+                                              : sub * 8 + e;
+                    const double a = p * s_invf[j];
                     const double nrev = rint(a * 0.15915494309189535);
                     double red = fma(-nrev, 6.283185307179586, a);
                     red = fma(-nrev, 2.4492935982947064e-16, red);
@@ -248,7 +276,10 @@ __global__ __launch_bounds__(kInjThreads) void inject_kernel(
 #pragma unroll
             for (int j = 0; j < kUnroll; ++j) {
                 uint4 ylo, yhi;
-                rotate8(klo[j], khi[j], cs, sn, ylo, yhi);
+                if (INTERLEAVED)
+                    rotate8_interleaved(klo[j], khi[j], cs, sn, ylo, yhi);
+                else
+                    rotate8(klo[j], khi[j], cs, sn, ylo, yhi);
                 if (l + j < l1) {
                     const int64_t dj = (int64_t)(l + j) * dstride;
                     kdst[dj] = ylo;
@@ -269,7 +300,8 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
                          int32_t k, int32_t nq, int64_t n, int64_t lens_stride,
                          int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
-                         int64_t T_store, int64_t num_slots, uint32_t* status, hipStream_t st) {
+                         int64_t T_store, int64_t num_slots, const double* inv_freq,
+                         int32_t interleaved, uint32_t* status, hipStream_t st) {
     const int64_t U = (int64_t)H * (D >> 4);
     const int64_t ntb_max = ((int64_t)max_tokens * U + kInjThreads - 1) / kInjThreads;
     if (ntb_max == 0) return hipSuccess;
@@ -281,10 +313,18 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     if (per_req > ntb_max * L) per_req = ntb_max * L;
     if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
-    hipLaunchKernelGGL(inject_kernel, grid, dim3(kInjThreads), 0, st, ids, (const uint4*)preK,
-                       (const uint4*)V, slots, positions, rope_theta, (uint4*)paged_k,
-                       (uint4*)paged_v, fact_offsets, fact_lens, m, k, n, lens_stride,
-                       reverse_rank, max_tokens, L, H, D, T_store, num_slots, status);
+    if (interleaved)
+        hipLaunchKernelGGL(inject_kernel<true>, grid, dim3(kInjThreads), 0, st, ids,
+                           (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
+                           (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
+                           lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+                           inv_freq, status);
+    else
+        hipLaunchKernelGGL(inject_kernel<false>, grid, dim3(kInjThreads), 0, st, ids,
+                           (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
+                           (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
+                           lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+                           inv_freq, status);
     return hipGetLastError();
 }
 

@@ -53,6 +53,7 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
                          int32_t k, int32_t nq, int64_t n, int64_t lens_stride,
                          int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
-                         int64_t T_store, int64_t num_slots, uint32_t* status, hipStream_t st);
+                         int64_t T_store, int64_t num_slots, const double* inv_freq,
+                         int32_t interleaved, uint32_t* status, hipStream_t st);
 
 }  // namespace is

@@ -5,8 +5,8 @@ from __future__ import annotations
 
 import torch
 
-from . import (IS_DTYPE_BF16, IS_DTYPE_F32, is_inject, is_retrieve,
-               is_retrieve_workspace_size, is_slot_map)
+from . import (IS_DTYPE_BF16, IS_DTYPE_F32, IS_ROPE_HALF_SPLIT, is_inject, is_inject_rotary,
+               is_retrieve, is_retrieve_workspace_size, is_slot_map)
 
 
 class RequestBuffers:
@@ -46,18 +46,24 @@ class RequestBuffers:
                     stream=stream)
 
     def inject(self, preK, V, rope_theta, paged_k, paged_v, *, fact_offsets, fact_lens,
-               lens_stride, reverse_rank=1, stream=None):
+               lens_stride, reverse_rank=1, inv_freq=None, pairing=IS_ROPE_HALF_SPLIT,
+               stream=None):
         L, T_store, H, D = preK.shape
-        is_inject(self.ids, preK, V, self.slots, self.positions, rope_theta, paged_k, paged_v,
-                  fact_offsets=fact_offsets, fact_lens=fact_lens, m=self.m, k=self.k,
+        kw = dict(fact_offsets=fact_offsets, fact_lens=fact_lens, m=self.m, k=self.k,
                   nq=self.nq, n=self.n, lens_stride=lens_stride, reverse_rank=reverse_rank,
                   max_tokens=self.max_tokens, L=L, H=H, D=D, T_store=T_store,
                   num_slots=paged_k.shape[1], status=self.status, stream=stream)
+        if inv_freq is None and pairing == IS_ROPE_HALF_SPLIT:
+            is_inject(self.ids, preK, V, self.slots, self.positions, rope_theta, paged_k,
+                      paged_v, **kw)
+        else:
+            is_inject_rotary(self.ids, preK, V, self.slots, self.positions, rope_theta, paged_k,
+                             paged_v, inv_freq=inv_freq, pairing=pairing, **kw)
 
 
 def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, paged_v, *,
                 start_pos, page_size, rope_theta, shared_bank=True, reverse_rank=1,
-                stream=None):
+                inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, stream=None):
     """Enqueue retrieve -> slot map -> inject for every request of ``buf``.
 
     ``store`` is a dict with preK, V ([L][T_store][H][D] bf16), fact_lens
@@ -70,4 +76,5 @@ def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, p
                  reverse_rank=reverse_rank, stream=stream)
     buf.inject(store["preK"], store["V"], rope_theta, paged_k, paged_v,
                fact_offsets=store["fact_offsets"], fact_lens=store["fact_lens"],
-               lens_stride=lens_stride, reverse_rank=reverse_rank, stream=stream)
+               lens_stride=lens_stride, reverse_rank=reverse_rank, inv_freq=inv_freq,
+               pairing=pairing, stream=stream)

@@ -44,11 +44,18 @@ class Instance:
         self.buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=self.bank.dtype,
                                   max_tokens=self.max_tokens, device=device)
 
-    def run(self, reverse_rank=1):
+    def run(self, reverse_rank=1, inv_freq=None, interleaved=False):
+        """One pass; inv_freq (float64 numpy [D/2]) and interleaved select the
+        rotary table and pair layout (kept for the checks)."""
+        from paper_2607_27090_amd import IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED
         w = self.w
+        self.inv_freq, self.interleaved = inv_freq, bool(interleaved)
+        tf = None if inv_freq is None else torch.from_numpy(np.ascontiguousarray(
+            inv_freq, dtype=np.float64)).cuda()
         run_request(self.buf, self.query, self.bank, self.store, self.bt, self.pk, self.pv,
                     start_pos=w.start_pos, page_size=w.page_size, rope_theta=w.theta,
-                    shared_bank=w.shared_bank, reverse_rank=reverse_rank)
+                    shared_bank=w.shared_bank, reverse_rank=reverse_rank, inv_freq=tf,
+                    pairing=IS_ROPE_INTERLEAVED if interleaved else IS_ROPE_HALF_SPLIT)
         torch.cuda.synchronize()
 
     # ---- checks --------------------------------------------------------------
@@ -123,7 +130,8 @@ class Instance:
         hv = hk.copy()
         st = oracle.inject(gids, Kc, Vc, o["slots"], o["positions"], w.theta, hk, hv, coffs,
                            lens, o["m"], w.k, w.nq, w.n, lens_stride, 1, self.max_tokens, L, H, D,
-                           cur, self.num_slots)
+                           cur, self.num_slots, inv_freq=getattr(self, "inv_freq", None),
+                           interleaved=getattr(self, "interleaved", False))
         assert st == 0
         gk, gv = u16(self.pk), u16(self.pv)
         assert np.array_equal(gv, hv), "V pages differ"
@@ -138,7 +146,8 @@ class Instance:
             m = o["m"][r]
             src = coffs_rows(o, r, coffs, lens_stride)
             pre[:, o["slots"][r, :m]] = Kc[:, src]
-        floor = parity.check_k_rows(gk[:, touched], hk[:, touched], pre[:, touched], D)
+        floor = parity.check_k_rows(gk[:, touched], hk[:, touched], pre[:, touched], D,
+                                    getattr(self, "interleaved", False))
         return floor
 
     def check_inject_sampled(self, frac=0.01, seed=0, max_rows=20000):

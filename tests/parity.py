@@ -44,16 +44,23 @@ def check_scores(gpu_scores: np.ndarray, s_star: np.ndarray, mag: np.ndarray):
     assert ok.all(), f"score mismatch: worst {err[~ok].max()} at {np.nonzero(~ok)[0][:5]}"
 
 
-def check_k_rows(gpu_bits: np.ndarray, ora_bits: np.ndarray, pre_bits: np.ndarray, D: int):
+def check_k_rows(gpu_bits: np.ndarray, ora_bits: np.ndarray, pre_bits: np.ndarray, D: int,
+                 interleaved: bool = False):
     """Rows [..., H*D] (or [..., H, D]) of rotated keys; pre_bits the
-    unrotated input rows of the same shape. Returns the count of elements
-    that needed the pair-norm floor."""
+    unrotated input rows of the same shape; interleaved: pairs (2j, 2j+1)
+    instead of (j, j + D/2). Returns the count of elements that needed the
+    pair-norm floor."""
     g = gpu_bits.reshape(-1, D)
     o = ora_bits.reshape(-1, D)
     x = oracle.bf16_to_f64(pre_bits.reshape(-1, D))
     half = D // 2
-    pair = np.hypot(x[:, :half], x[:, half:])
-    pair = np.concatenate([pair, pair], axis=1)
+    if interleaved:
+        pn = np.hypot(x[:, 0::2], x[:, 1::2])
+        pair = np.empty_like(x)
+        pair[:, 0::2], pair[:, 1::2] = pn, pn
+    else:
+        pair = np.hypot(x[:, :half], x[:, half:])
+        pair = np.concatenate([pair, pair], axis=1)
     if np.array_equal(g, o):
         return 0
     ulp = np.abs(ordered_bf16(g) - ordered_bf16(o))
