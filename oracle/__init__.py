@@ -13,7 +13,9 @@ Paper passages followed (InferScale):
   * slots: §2.2 paged KV cache (fixed-size blocks through a block table);
   * rotation: §2.4 and Theorem "Chunked RoPE Injection" (§5.1); with the
     model's own rotary table and pair layout, §3.3 and §6.1;
-  * composition and scatter: §3.3 and §3.4.
+  * composition and scatter: §3.3 and §3.4;
+  * the consumer of the pages (attention logits of the query that follows
+    the memory): Theorem "Chunked RoPE Injection", §5.1.
 """
 from __future__ import annotations
 
@@ -87,6 +89,9 @@ def _load():
     lib.oracle_inject_rotary.argtypes = [P, P, P, P, P, f64, P, P, P, P, P, i32, i32, i64, i64,
                                          i32, i32, i32, i32, i32, i64, i64, P, i32, P]
     lib.oracle_inject_rotary.restype = ctypes.c_int
+    lib.oracle_paged_scores.argtypes = [P, P, P, i32, P, i32, i32, P, f64, P, i32, i32, i32,
+                                        i32, i32, i64, i32, i32, P, P]
+    lib.oracle_paged_scores.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -262,3 +267,28 @@ def inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, fact_of
     if rc != 0:
         raise ValueError(f"oracle_inject rejected its arguments (rc={rc})")
     return int(status[0])
+
+
+def paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, m, rope_theta,
+                 nq, Hq, H, D, num_slots, max_blocks, max_tokens, inv_freq=None,
+                 interleaved=False):
+    """Attention logits of each request's query (rotated to qpos[r]) against
+    its placed tokens' keys read through the block table; float64
+    [nq][Hq][max_tokens], NaN beyond m. Returns (scores, status)."""
+    lib = _load()
+    q_ = _c(q, np.uint16)
+    qp = _c(qpos, np.int32)
+    pk = _c(paged_k, np.uint16)
+    bt = _c(block_table, np.int32)
+    mm = _c(m, np.int32)
+    f = None if inv_freq is None else _c(inv_freq, np.float64)
+    out = np.full((nq, Hq, max_tokens), np.nan)
+    status = np.zeros((1,), dtype=np.uint32)
+    rc = lib.oracle_paged_scores(_ptr(q_), _ptr(qp), _ptr(pk), layer, _ptr(bt), page_size,
+                                 start_pos, _ptr(mm), float(rope_theta), _ptr(f),
+                                 int(bool(interleaved)), nq, Hq, H, D, num_slots, max_blocks,
+                                 max_tokens, _ptr(out), _ptr(status))
+    if rc != 0:
+        raise ValueError(f"oracle_paged_scores rejected its arguments (rc={rc})")
+    return out, int(status[0])
+

@@ -377,3 +377,57 @@ int oracle_inject(const int32_t* ids, const uint16_t* preK, const uint16_t* V,
                                 fact_offsets, fact_lens, m, k, nq, n, lens_stride, reverse_rank,
                                 max_tokens, L, H, D, T_store, num_slots, NULL, 0, status);
 }
+
+/* ---- the consumer of the pages: attention logits (Theorem "Chunked RoPE
+ * Injection", §5.1; §3.4; §3.3: the query follows the memory) ----------------
+ * For request r, query head hq (kv head hq / (Hq / H)), placed token idx <
+ * m[r] at position p = start_pos + idx:
+ *   scores[r][hq][idx] = sum_j (R_{qpos[r]} q[r][hq])_j * K[layer][slot(p)][hq/G][j]
+ * with slot(p) = block_table[r][p / P] * P + p mod P, the rotation as in
+ * oracle_rope_table_f64 (NULL table: rope_theta's default), in binary64 on
+ * the decoded bf16 inputs. Tokens whose block is beyond max_blocks, negative,
+ * or whose slot is outside the pool are skipped and flagged (BT_SHORT,
+ * BAD_BLOCK, SLOT_RANGE); their scores are left untouched. */
+int oracle_paged_scores(const uint16_t* q, const int32_t* qpos, const uint16_t* paged_k,
+                        int32_t layer, const int32_t* block_table, int32_t page_size,
+                        int32_t start_pos, const int32_t* m, double rope_theta,
+                        const double* inv_freq, int32_t interleaved, int32_t nq, int32_t Hq,
+                        int32_t H, int32_t D, int64_t num_slots, int32_t max_blocks,
+                        int32_t max_tokens, double* scores, uint32_t* status)
+{
+    if (!q || !qpos || !paged_k || !block_table || !m || !scores) return -1;
+    if (nq < 1 || H < 1 || Hq < H || Hq % H || D < 2 || D % 2 || D > 1024 || page_size < 1)
+        return -1;
+    double freq[512], xq[1024], rq[1024];
+    if (inv_freq)
+        for (int32_t j = 0; j < D / 2; ++j) freq[j] = inv_freq[j];
+    else
+        oracle_default_inv_freq(rope_theta, D, freq);
+    const int32_t G = Hq / H;
+    uint32_t flags = 0;
+    for (int32_t r = 0; r < nq; ++r) {
+        int32_t mr = m[r] < max_tokens ? m[r] : max_tokens;
+        for (int32_t hq = 0; hq < Hq; ++hq) {
+            const uint16_t* qv = q + ((int64_t)r * Hq + hq) * D;
+            for (int32_t e = 0; e < D; ++e) xq[e] = oracle_bf16_to_double(qv[e]);
+            oracle_rope_table_f64(xq, (double)qpos[r], freq, D, interleaved, rq);
+            for (int32_t idx = 0; idx < mr; ++idx) {
+                int64_t p = (int64_t)start_pos + idx;
+                int64_t blk = p / page_size;
+                if (blk >= max_blocks) { flags |= ORACLE_BT_SHORT; continue; }
+                int32_t b = block_table[(int64_t)r * max_blocks + blk];
+                if (b < 0) { flags |= ORACLE_BAD_BLOCK; continue; }
+                int64_t slot = (int64_t)b * page_size + p % page_size;
+                if (slot >= num_slots) { flags |= ORACLE_SLOT_RANGE; continue; }
+                const uint16_t* kv =
+                    paged_k + (((int64_t)layer * num_slots + slot) * H + hq / G) * D;
+                double acc = 0.0;
+                for (int32_t j = 0; j < D; ++j) acc += rq[j] * oracle_bf16_to_double(kv[j]);
+                scores[((int64_t)r * Hq + hq) * max_tokens + idx] = acc;
+            }
+        }
+    }
+    if (status) *status |= flags;
+    return 0;
+}
+
