@@ -217,6 +217,42 @@ int is_inject_rotary(const int32_t* ids, const void* preK, const void* V, const 
                      int64_t num_slots, const double* inv_freq, int32_t pairing, uint32_t* status,
                      void* stream);
 
+/*
+ * is_paged_scores -- the consumer of the injected pages: attention logits of
+ * each request's query against the keys of its placed tokens, read back
+ * through the request's block table (Theorem "Chunked RoPE Injection", §5.1:
+ * a key rotated at position p scores against a query at position N as the
+ * stored key would at relative position p - N; §3.3: the query follows the
+ * memory). For request r, query head hq, placed token idx < m[r]:
+ *   pos   = start_pos + idx
+ *   slot  = block_table[r][pos / page_size] * page_size + pos % page_size
+ *   scores[r][hq][idx] = sum_j (R_qpos[r] q[r][hq])_j * paged_k[layer][slot][hq / (Hq/H)][j]
+ * R rotates with inv_freq / pairing exactly as is_inject_rotary (NULL: the
+ * default table of rope_theta); the query rotation uses fp64-reduced angles
+ * and fp32 sine/cosine, the products and sums are fp32.
+ *
+ *   q            bf16 [nq][Hq][D] pre-RoPE queries, device
+ *   qpos         int32 [nq] query positions (start_pos + m[r] for the
+ *                position right after the memory)
+ *   paged_k      bf16 [L][num_slots][H][D] as written by is_inject, 16-byte
+ *                aligned; layer < L selects the layer
+ *   block_table  int32 [nq][max_blocks]; m int32 [nq] (as for is_slot_map)
+ *   scores       fp32 [nq][Hq][max_tokens], device; entries idx >= m[r] (and
+ *                skipped tokens) are not written
+ *   Hq           query heads: a multiple of H with Hq / H <= 8 and
+ *                Hq * D <= 8192
+ *   D            16, 32, 64, 128, 256 or 512
+ * Tokens whose block lies beyond max_blocks, is negative or maps outside
+ * [0, num_slots) are skipped and flagged (IS_DEV_BT_SHORT, IS_DEV_BAD_BLOCK,
+ * IS_DEV_SLOT_RANGE).
+ */
+int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int32_t layer,
+                    const int32_t* block_table, int32_t page_size, int32_t start_pos,
+                    const int32_t* m, float* scores, int32_t nq, int32_t Hq, int32_t H, int32_t D,
+                    int32_t L, int64_t num_slots, int32_t max_blocks, int32_t max_tokens,
+                    float rope_theta, const double* inv_freq, int32_t pairing, uint32_t* status,
+                    void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -40,7 +40,7 @@ IS_ROPE_HALF_SPLIT = 0
 IS_ROPE_INTERLEAVED = 1
 
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_slot_map", "is_inject", "is_inject_rotary")
+            "is_slot_map", "is_inject", "is_inject_rotary", "is_paged_scores")
 
 
 class InferScaleError(RuntimeError):
@@ -79,6 +79,9 @@ def load_library() -> ctypes.CDLL:
     lib.is_inject_rotary.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32,
                                      i32, i32, i32, i32, i64, i64, P, i32, P, P]
     lib.is_inject_rotary.restype = ctypes.c_int
+    lib.is_paged_scores.argtypes = [P, P, P, i32, P, i32, i32, P, P, i32, i32, i32, i32, i32,
+                                    i64, i32, i32, f32, P, i32, P, P]
+    lib.is_paged_scores.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -192,3 +195,17 @@ def is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_
         float(rope_theta), _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens),
         _ptr(m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
         _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
+
+
+def is_paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, m, scores, *,
+                    nq, Hq, H, D, L, num_slots, max_blocks, max_tokens, rope_theta,
+                    inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
+    """Attention logits of each request's query against its injected keys
+    read through the block table (see include/inferscale.h)."""
+    if inv_freq is not None and inv_freq.dtype != torch.float64:
+        raise ValueError("inv_freq must be a float64 tensor")
+    _check("is_paged_scores", load_library().is_paged_scores(
+        _ptr(q), _ptr(qpos), _ptr(paged_k), layer, _ptr(block_table), page_size, start_pos,
+        _ptr(m), _ptr(scores), nq, Hq, H, D, L, num_slots, max_blocks, max_tokens,
+        float(rope_theta), _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
+

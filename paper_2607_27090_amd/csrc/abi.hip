@@ -333,4 +333,44 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
                             status, stream);
 }
 
+int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int32_t layer,
+                    const int32_t* block_table, int32_t page_size, int32_t start_pos,
+                    const int32_t* m, float* scores, int32_t nq, int32_t Hq, int32_t H, int32_t D,
+                    int32_t L, int64_t num_slots, int32_t max_blocks, int32_t max_tokens,
+                    float rope_theta, const double* inv_freq, int32_t pairing, uint32_t* status,
+                    void* stream) {
+    if (!q || !qpos || !paged_k || !block_table || !m || !scores)
+        return fail(IS_ERR_INVALID, "q, qpos, paged_k, block_table, m and scores must be non-NULL");
+    if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
+    if (H < 1 || Hq < H || Hq % H || Hq / H > is::consumer_max_group())
+        return fail(IS_ERR_UNSUPPORTED, "Hq=%d must be a multiple of H=%d with Hq/H <= %d", Hq, H,
+                    is::consumer_max_group());
+    if (D < 16 || D > IS_MAX_HEAD_DIM || (D & (D - 1)))
+        return fail(IS_ERR_UNSUPPORTED, "D=%d must be a power of two in [16, %d]", D,
+                    IS_MAX_HEAD_DIM);
+    if ((int64_t)Hq * D > is::consumer_max_q_elems())
+        return fail(IS_ERR_UNSUPPORTED, "Hq*D=%lld exceeds %d", (long long)Hq * D,
+                    is::consumer_max_q_elems());
+    if (L < 1 || layer < 0 || layer >= L)
+        return fail(IS_ERR_INVALID, "layer=%d must be in [0, L=%d)", layer, L);
+    if (page_size < 1 || max_blocks < 1 || max_tokens < 0 || num_slots < 0 || start_pos < 0)
+        return fail(IS_ERR_INVALID, "page_size and max_blocks must be >= 1; max_tokens, "
+                                    "num_slots and start_pos >= 0");
+    if (!inv_freq && (!(rope_theta > 0.f) || !std::isfinite(rope_theta)))
+        return fail(IS_ERR_INVALID, "rope_theta must be positive and finite");
+    if (pairing != IS_ROPE_HALF_SPLIT && pairing != IS_ROPE_INTERLEAVED)
+        return fail(IS_ERR_INVALID, "pairing=%d is neither IS_ROPE_HALF_SPLIT nor IS_ROPE_INTERLEAVED",
+                    pairing);
+    if (!aligned(paged_k, 16) || !aligned(q, 2) || !aligned(scores, 4) || !aligned(qpos, 4) ||
+        !aligned(block_table, 4) || !aligned(m, 4) || (status && !aligned(status, 4)) ||
+        (inv_freq && !aligned(inv_freq, 8)))
+        return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    hipError_t e = is::launch_paged_scores(q, qpos, paged_k, layer, block_table, page_size,
+                                           start_pos, m, scores, nq, Hq, H, D, num_slots,
+                                           max_blocks, max_tokens, rope_theta, inv_freq, pairing,
+                                           status, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "paged scores launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
 }  // extern "C"

@@ -56,4 +56,15 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          int64_t T_store, int64_t num_slots, const double* inv_freq,
                          int32_t interleaved, uint32_t* status, hipStream_t st);
 
+// consumer.hip
+int consumer_max_q_elems();
+int consumer_max_group();
+hipError_t launch_paged_scores(const void* q, const int32_t* qpos, const void* paged_k,
+                               int32_t layer, const int32_t* block_table, int32_t page_size,
+                               int32_t start_pos, const int32_t* m, float* scores, int32_t nq,
+                               int32_t Hq, int32_t H, int32_t D, int64_t num_slots,
+                               int32_t max_blocks, int32_t max_tokens, float rope_theta,
+                               const double* inv_freq, int32_t interleaved, uint32_t* status,
+                               hipStream_t st);
+
 }  // namespace is
