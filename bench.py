@@ -61,6 +61,9 @@ def parse():
                     help="rotary table / pair layout of the inject: theta^(-2j/D) half-split "
                          "(is_inject), Llama 3.1's scaled table, or interleaved pairs "
                          "(is_inject_rotary)")
+    ap.add_argument("--consumer", action="store_true",
+                    help="also time is_paged_scores (attention logits of a query after the "
+                         "memory, 4 query heads per KV head) over every layer of each request")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -76,7 +79,7 @@ def main():
     import torch
     import workloads
     from paper_2607_27090_amd import (IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED, is_inject,
-                                      is_inject_rotary, is_slot_map)
+                                      is_inject_rotary, is_paged_scores, is_slot_map)
     from paper_2607_27090_amd.pipeline import RequestBuffers
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -208,6 +211,31 @@ def main():
     torch.cuda.synchronize()
     inj_launch_ms = ei0.elapsed_time(ei1) / (args.steps * nwaves)
     log(f"inject alone: {inj_launch_ms * 1e3:.1f} us per launch")
+
+    # ---- optional: the consumer of the pages, every layer of every request ---
+    consumer = None
+    if args.consumer and nwaves == 1:
+        Hq = 4 * w.H
+        gq = torch.Generator(device=dev).manual_seed(99)
+        qc = torch.randn(w.nq, Hq, w.D, generator=gq, device=dev).to(torch.bfloat16)
+        sc = torch.empty(w.nq, Hq, w.max_tokens, device=dev)
+        qpos = [(sets[si].m + w.start_pos).to(torch.int32) for si in range(args.steps)]
+        ec0, ec1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ec0.record()
+        for si, i in enumerate(range(args.warmup, nsteps)):
+            for layer in range(w.L):
+                is_paged_scores(qc, qpos[si], pk, layer, bts[(i * nwaves) % R], w.page_size,
+                                w.start_pos, sets[si].m, sc, nq=w.nq, Hq=Hq, H=H, D=D, L=L,
+                                num_slots=num_slots, max_blocks=bts.shape[-1],
+                                max_tokens=w.max_tokens, rope_theta=w.theta,
+                                status=sets[si].status)
+        ec1.record()
+        torch.cuda.synchronize()
+        cons_ms = ec0.elapsed_time(ec1) / (args.steps * w.L)
+        cons_bytes = statistics.fmean(int(b.m.sum()) for b in sets) * (H * D * 2 + Hq * 4)
+        consumer = {"us_per_layer": round(cons_ms * 1e3, 2), "query_heads": Hq,
+                    "GBps": round(cons_bytes / (cons_ms * 1e-3) / 1e9, 1)}
+        log(f"consumer: {cons_ms * 1e3:.1f} us per layer, {consumer['GBps']} GB/s")
     latency_ms = None
     if args.detail and S > 1:
         latency_ms = timed(1) / args.steps
@@ -341,6 +369,7 @@ def main():
             "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
             "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
+        "consumer": consumer,
         "roofline": {
             "bound": "hbm",
             "kernel": "inject_kernel",
