@@ -125,3 +125,49 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         isl.is_retrieve(t, t, 4, 8, 1, torch.zeros(1, 1, dtype=torch.int32),
                         workspace=torch.zeros(256, dtype=torch.uint8))
+
+
+def _rotary(**kw):
+    a = dict(ids=A, K=A, V=A, slots=A, pos=A, theta=500000.0, pk=A, pv=A, offs=A, lens=A, m=A,
+             k=5, nq=1, n=100, ls=0, rev=1, mt=100, L=2, H=8, D=128, T=1000, ns=1000, f=None,
+             pairing=0, status=A)
+    a.update(kw)
+    return isl.load_library().is_inject_rotary(
+        a["ids"], a["K"], a["V"], a["slots"], a["pos"], a["theta"], a["pk"], a["pv"], a["offs"],
+        a["lens"], a["m"], a["k"], a["nq"], a["n"], a["ls"], a["rev"], a["mt"], a["L"], a["H"],
+        a["D"], a["T"], a["ns"], a["f"], a["pairing"], a["status"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(pairing=2), isl.IS_ERR_INVALID), (dict(pairing=-1), isl.IS_ERR_INVALID),
+    (dict(f=A + 4), isl.IS_ERR_INVALID), (dict(theta=0.0), isl.IS_ERR_INVALID),
+    (dict(ids=None), isl.IS_ERR_INVALID), (dict(D=24), isl.IS_ERR_UNSUPPORTED),
+    # no table: theta must be valid; the pointer check refuses a fake store
+    (dict(theta=float("nan")), isl.IS_ERR_INVALID), (dict(), isl.IS_ERR_INVALID),
+])
+def test_inject_rotary_rejects(kw, code):
+    assert _rotary(**kw) == code
+
+
+def _scores(**kw):
+    a = dict(q=A, qpos=A, pk=A, layer=0, bt=A, P=16, start=0, m=A, sc=A, nq=1, Hq=32, H=8,
+             D=128, L=2, ns=1000, mb=10, mt=100, theta=500000.0, f=None, pairing=0, status=A)
+    a.update(kw)
+    return isl.load_library().is_paged_scores(
+        a["q"], a["qpos"], a["pk"], a["layer"], a["bt"], a["P"], a["start"], a["m"], a["sc"],
+        a["nq"], a["Hq"], a["H"], a["D"], a["L"], a["ns"], a["mb"], a["mt"], a["theta"], a["f"],
+        a["pairing"], a["status"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), isl.IS_ERR_INVALID), (dict(sc=None), isl.IS_ERR_INVALID),
+    (dict(nq=0), isl.IS_ERR_INVALID), (dict(Hq=12), isl.IS_ERR_UNSUPPORTED),
+    (dict(Hq=8 * 9), isl.IS_ERR_UNSUPPORTED), (dict(D=96), isl.IS_ERR_UNSUPPORTED),
+    (dict(D=8), isl.IS_ERR_UNSUPPORTED), (dict(Hq=64, D=256), isl.IS_ERR_UNSUPPORTED),
+    (dict(layer=2), isl.IS_ERR_INVALID), (dict(layer=-1), isl.IS_ERR_INVALID),
+    (dict(P=0), isl.IS_ERR_INVALID), (dict(mb=0), isl.IS_ERR_INVALID),
+    (dict(theta=0.0), isl.IS_ERR_INVALID), (dict(pairing=3), isl.IS_ERR_INVALID),
+    (dict(pk=A + 8), isl.IS_ERR_INVALID), (dict(f=A + 4), isl.IS_ERR_INVALID),
+])
+def test_paged_scores_rejects(kw, code):
+    assert _scores(**kw) == code
