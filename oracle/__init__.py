@@ -15,7 +15,9 @@ Paper passages followed (InferScale):
     model's own rotary table and pair layout, §3.3 and §6.1;
   * composition and scatter: §3.3 and §3.4;
   * the consumer of the pages (attention logits of the query that follows
-    the memory): Theorem "Chunked RoPE Injection", §5.1.
+    the memory): Theorem "Chunked RoPE Injection", §5.1;
+  * the graph-ANN backend (proximity graph and beam search, §2.6 and §6.1)
+    in ``ann.c``, with the readings stated at its top.
 """
 from __future__ import annotations
 
@@ -27,6 +29,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "ann.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 F32 = 0
@@ -44,9 +47,10 @@ _lib = None
 
 
 def build() -> str:
-    """Compile oracle.c into liboracle.so with gcc (strict IEEE, no fast-math)."""
+    """Compile oracle.c and ann.c into liboracle.so with gcc (strict IEEE, no
+    fast-math)."""
     cmd = ["gcc", "-O2", "-fPIC", "-shared", "-fno-fast-math", "-ffp-contract=off",
-           "-std=c11", "-Wall", "-Wno-maybe-uninitialized", "-o", _LIB, _SRC, "-lm"]
+           "-std=c11", "-Wall", "-Wno-maybe-uninitialized", "-o", _LIB, *_SRCS, "-lm"]
     subprocess.run(cmd, check=True)
     return _LIB
 
@@ -55,7 +59,7 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(map(os.path.getmtime, _SRCS)):
         build()
     lib = ctypes.CDLL(_LIB)
     P = ctypes.c_void_p
@@ -92,6 +96,15 @@ def _load():
     lib.oracle_paged_scores.argtypes = [P, P, P, i32, P, i32, i32, P, f64, P, i32, i32, i32,
                                         i32, i32, i64, i32, i32, P, P]
     lib.oracle_paged_scores.restype = ctypes.c_int
+    lib.oracle_ann_knn.argtypes = [P, i64, i32, i32, i32, P]
+    lib.oracle_ann_knn.restype = ctypes.c_int
+    lib.oracle_ann_merge.argtypes = [P, i64, i32, P]
+    lib.oracle_ann_merge.restype = ctypes.c_int
+    lib.oracle_ann_build.argtypes = [P, i64, i32, i32, i32, P, P]
+    lib.oracle_ann_build.restype = ctypes.c_int
+    lib.oracle_ann_search.argtypes = [P, i32, P, i64, i32, i32, P, i32, P, i32, i32, i32, i32,
+                                      i32, P, P, P, P]
+    lib.oracle_ann_search.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -292,3 +305,68 @@ def paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, m, 
         raise ValueError(f"oracle_paged_scores rejected its arguments (rc={rc})")
     return out, int(status[0])
 
+
+
+# ---- graph-ANN backend (ann.c) ---------------------------------------------
+
+def _emb(a, dtype):
+    return _c(a, np.float32 if dtype == F32 else np.uint16)
+
+
+def ann_knn(bank, n, d, R, dtype=F32) -> np.ndarray:
+    """Forward lists F [n][R]: the R best j != i by inner product, best first,
+    equal scores to the lower id."""
+    lib = _load()
+    b = _emb(bank, dtype)
+    F = np.empty((n, R), dtype=np.int32)
+    rc = lib.oracle_ann_knn(_ptr(b), n, d, dtype, R, _ptr(F))
+    if rc != 0:
+        raise ValueError(f"oracle_ann_knn rejected its arguments (rc={rc})")
+    return F
+
+
+def ann_merge(F) -> np.ndarray:
+    """Final lists G [n][R] from forward lists F (forward half, reverse edges,
+    forward fill)."""
+    lib = _load()
+    F_ = _c(F, np.int32)
+    n, R = F_.shape
+    G = np.empty((n, R), dtype=np.int32)
+    rc = lib.oracle_ann_merge(_ptr(F_), n, R, _ptr(G))
+    if rc != 0:
+        raise ValueError(f"oracle_ann_merge rejected its arguments (rc={rc})")
+    return G
+
+
+def ann_build(bank, n, d, R, dtype=F32):
+    """(F, G): forward lists and final graph."""
+    lib = _load()
+    b = _emb(bank, dtype)
+    F = np.empty((n, R), dtype=np.int32)
+    G = np.empty((n, R), dtype=np.int32)
+    rc = lib.oracle_ann_build(_ptr(b), n, d, dtype, R, _ptr(F), _ptr(G))
+    if rc != 0:
+        raise ValueError(f"oracle_ann_build rejected its arguments (rc={rc})")
+    return F, G
+
+
+def ann_search(query, bank, n, d, graph, seeds, beam, k, max_iters, width=1, dtype=F32):
+    """Beam search: returns dict(ids int32 [nq][k], scores float64 [nq][k],
+    iters int32 [nq], status)."""
+    lib = _load()
+    q = _emb(query, dtype)
+    nq = q.size // d
+    b = _emb(bank, dtype)
+    g = _c(graph, np.int32)
+    R = g.shape[1]
+    s = _c(seeds, np.int32)
+    ids = np.empty((nq, k), dtype=np.int32)
+    vals = np.empty((nq, k), dtype=np.float64)
+    iters = np.empty((nq,), dtype=np.int32)
+    status = np.zeros((1,), dtype=np.uint32)
+    rc = lib.oracle_ann_search(_ptr(q), nq, _ptr(b), n, d, dtype, _ptr(g), R, _ptr(s), s.size,
+                               beam, width, k, max_iters, _ptr(ids), _ptr(vals), _ptr(iters),
+                               _ptr(status))
+    if rc != 0:
+        raise ValueError(f"oracle_ann_search rejected its arguments (rc={rc})")
+    return dict(ids=ids, scores=vals, iters=iters, status=int(status[0]))
