@@ -77,6 +77,12 @@ extern "C" {
 #define IS_MAX_K 1024         /* largest k                                           */
 #define IS_MAX_HEAD_DIM 512   /* largest head dimension D                            */
 
+/* graph-ANN limits */
+#define IS_ANN_MAX_DEGREE 128 /* out-degree of the proximity graph                   */
+#define IS_ANN_MAX_BEAM 256   /* beam width                                          */
+#define IS_ANN_MAX_WIDTH 4    /* beam entries expanded per iteration                 */
+#define IS_ANN_MAX_EXPAND 256 /* width * degree                                      */
+
 /* Library version string, e.g. "inferscale-gfx950 0.1.0". */
 const char* is_version(void);
 
@@ -252,6 +258,92 @@ int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int
                     int32_t L, int64_t num_slots, int32_t max_blocks, int32_t max_tokens,
                     float rope_theta, const double* inv_freq, int32_t pairing, uint32_t* status,
                     void* stream);
+
+/*
+ * Graph-ANN retrieval: the paper's vector backend is a GPU-resident
+ * proximity graph over the fact embeddings, answered by a beam search on the
+ * device (§2.6; §6.1: inner product, 64 neighbours, beam width 64). The
+ * paper fixes those parameters only; the construction and the search loop
+ * below are this library's reading. It is an alternative to is_retrieve for
+ * banks too large to scan per request: the search reads the rows of the
+ * facts it visits instead of the whole bank, and returns the exact top-k
+ * only when the beam reaches it.
+ *
+ * Order: a fact ranks above another when its score (fp32 inner product, as
+ * for is_retrieve) is higher, or equal with a lower id.
+ */
+
+/* Bytes of device workspace is_ann_build needs (0 on bad arguments). */
+int is_ann_build_workspace_size(int64_t n, int32_t d, int32_t degree, int32_t dtype,
+                                size_t* bytes);
+
+/*
+ * is_ann_build -- the proximity graph (out-degree R = degree, h = R / 2):
+ *   F[i]   = the R facts j != i ranked highest for query x_i (exact, by the
+ *            retrieval kernels of is_retrieve, k = R + 1 with i removed);
+ *   rev(i) = the facts j with i among F[j][0 .. h), ordered by the position
+ *            of i in F[j], then by j;
+ *   G[i]   = F[i][0 .. h), then the first R - h facts of rev(i) that F[i]
+ *            does not already list there, then F[i][h .. R) in order without
+ *            the facts already listed, until R facts are listed.
+ * The reverse edges keep facts that no forward list names reachable.
+ * Seeds (entry points of the search): seed_ids[s] = floor(s * n / n_seeds)
+ * and seed_bank[s] = bank[seed_ids[s]], a contiguous copy of their rows.
+ *
+ *   bank       [n][d] of dtype, 16-byte aligned; 2 <= n < 2^31;
+ *              d a multiple of 8 in [8, 8192]
+ *   degree     1 <= degree <= min(IS_ANN_MAX_DEGREE, n - 1)
+ *   n_seeds    0 <= n_seeds <= n (0: seed_ids and seed_bank are not written
+ *              and may be NULL)
+ *   graph      int32 [n][degree] device (output G)
+ *   fwd        int32 [n][degree] device (output F) or NULL
+ *   seed_ids   int32 [n_seeds] device; seed_bank [n_seeds][d] of dtype,
+ *              16-byte aligned
+ *   workspace  at least is_ann_build_workspace_size bytes, 256-byte aligned
+ * Cost: one exact retrieval per batch of 256 bank rows, then O(n * degree)
+ * for the reverse edges. Built once per bank, outside the request path
+ * (§6.1 counts index construction as offline set-up).
+ */
+int is_ann_build(const void* bank, int64_t n, int32_t d, int32_t degree, int32_t dtype,
+                 int32_t n_seeds, int32_t* graph, int32_t* fwd, int32_t* seed_ids,
+                 void* seed_bank, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace is_ann_search needs (0 on bad arguments). */
+int is_ann_search_workspace_size(int32_t n_seeds, int32_t d, int32_t beam, int32_t nq,
+                                 int32_t dtype, size_t* bytes);
+
+/*
+ * is_ann_search -- beam search over the graph, per query r:
+ *   the beam starts as the min(beam, n_seeds) best seeds (exact retrieval
+ *   over seed_bank), none expanded; each iteration takes the first `width`
+ *   unexpanded beam entries in rank order (none: stop), marks them
+ *   expanded, scores every neighbour of theirs not in the beam (each once)
+ *   and keeps the `beam` best of the old beam and those neighbours; at most
+ *   max_iters iterations. Output row r: the first k beam entries, best
+ *   first (id -1 and score -inf past the beam's end when it holds fewer
+ *   than k), and out_iters[r] = iterations run.
+ *
+ *   query_emb  [nq][d] of dtype, 16-byte aligned; 1 <= nq <= 65535
+ *   bank       [n][d] of dtype (the bank the graph was built on), 16-byte
+ *              aligned; rows of at most 8 KiB (d <= 2048 fp32, 4096 bf16)
+ *   graph      int32 [n][degree] (is_ann_build's G)
+ *   seed_ids   int32 [n_seeds] distinct ids; seed_bank [n_seeds][d] their
+ *              rows (is_ann_build's seeds); 1 <= n_seeds <= n
+ *   beam       1 <= beam <= IS_ANN_MAX_BEAM; 1 <= k <= beam
+ *   width      1 <= width <= IS_ANN_MAX_WIDTH, width * degree <=
+ *              IS_ANN_MAX_EXPAND
+ *   max_iters  >= 0 (0: the best seeds)
+ *   out_ids    int32 [nq][k]; out_scores fp32 [nq][k] or NULL; out_iters
+ *              int32 [nq] or NULL; all device
+ *   status     device flag word or NULL: a graph entry or seed id outside
+ *              [0, n) sets IS_DEV_ID_RANGE and is skipped
+ *   workspace  at least is_ann_search_workspace_size bytes, 256-byte aligned
+ */
+int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n, int32_t d,
+                  int32_t dtype, const int32_t* graph, int32_t degree, const int32_t* seed_ids,
+                  const void* seed_bank, int32_t n_seeds, int32_t beam, int32_t width, int32_t k,
+                  int32_t max_iters, int32_t* out_ids, float* out_scores, int32_t* out_iters,
+                  uint32_t* status, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -39,8 +39,15 @@ IS_MAX_HEAD_DIM = 512
 IS_ROPE_HALF_SPLIT = 0
 IS_ROPE_INTERLEAVED = 1
 
+IS_ANN_MAX_DEGREE = 128
+IS_ANN_MAX_BEAM = 256
+IS_ANN_MAX_WIDTH = 4
+IS_ANN_MAX_EXPAND = 256
+
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_slot_map", "is_inject", "is_inject_rotary", "is_paged_scores")
+            "is_slot_map", "is_inject", "is_inject_rotary", "is_paged_scores",
+            "is_ann_build_workspace_size", "is_ann_build", "is_ann_search_workspace_size",
+            "is_ann_search")
 
 
 class InferScaleError(RuntimeError):
@@ -82,6 +89,15 @@ def load_library() -> ctypes.CDLL:
     lib.is_paged_scores.argtypes = [P, P, P, i32, P, i32, i32, P, P, i32, i32, i32, i32, i32,
                                     i64, i32, i32, f32, P, i32, P, P]
     lib.is_paged_scores.restype = ctypes.c_int
+    lib.is_ann_build_workspace_size.argtypes = [i64, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.is_ann_build_workspace_size.restype = ctypes.c_int
+    lib.is_ann_build.argtypes = [P, i64, i32, i32, i32, i32, P, P, P, P, P, sz, P]
+    lib.is_ann_build.restype = ctypes.c_int
+    lib.is_ann_search_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.is_ann_search_workspace_size.restype = ctypes.c_int
+    lib.is_ann_search.argtypes = [P, i32, P, i64, i32, i32, P, i32, P, P, i32, i32, i32, i32,
+                                  i32, P, P, P, P, P, sz, P]
+    lib.is_ann_search.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -209,3 +225,48 @@ def is_paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, 
         _ptr(m), _ptr(scores), nq, Hq, H, D, L, num_slots, max_blocks, max_tokens,
         float(rope_theta), _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
 
+
+
+def is_ann_build_workspace_size(n: int, d: int, degree: int, dtype: int = IS_DTYPE_F32) -> int:
+    out = ctypes.c_size_t(0)
+    _check("is_ann_build_workspace_size",
+           load_library().is_ann_build_workspace_size(n, d, degree, dtype, ctypes.byref(out)))
+    return out.value
+
+
+def is_ann_build(bank, n, d, degree, graph, *, n_seeds=0, fwd=None, seed_ids=None,
+                 seed_bank=None, workspace=None, stream=None) -> None:
+    """Proximity graph over the bank, plus the search's seeds (see
+    include/inferscale.h)."""
+    dt = _emb_dtype(bank)
+    if workspace is None:
+        raise ValueError("is_ann_build needs a workspace tensor "
+                         "(is_ann_build_workspace_size bytes of device memory)")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("is_ann_build", load_library().is_ann_build(
+        _ptr(bank), n, d, degree, dt, n_seeds, _ptr(graph), _ptr(fwd), _ptr(seed_ids),
+        _ptr(seed_bank), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def is_ann_search_workspace_size(n_seeds: int, d: int, beam: int, nq: int = 1,
+                                 dtype: int = IS_DTYPE_F32) -> int:
+    out = ctypes.c_size_t(0)
+    _check("is_ann_search_workspace_size",
+           load_library().is_ann_search_workspace_size(n_seeds, d, beam, nq, dtype,
+                                                       ctypes.byref(out)))
+    return out.value
+
+
+def is_ann_search(query_emb, bank, n, d, graph, degree, seed_ids, seed_bank, out_ids, *,
+                  nq=1, n_seeds, beam=64, width=1, k, max_iters, out_scores=None, out_iters=None,
+                  status=None, workspace=None, stream=None) -> None:
+    """Beam search over the proximity graph (see include/inferscale.h)."""
+    dt = _emb_dtype(query_emb)
+    if workspace is None:
+        raise ValueError("is_ann_search needs a workspace tensor "
+                         "(is_ann_search_workspace_size bytes of device memory)")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("is_ann_search", load_library().is_ann_search(
+        _ptr(query_emb), nq, _ptr(bank), n, d, dt, _ptr(graph), degree, _ptr(seed_ids),
+        _ptr(seed_bank), n_seeds, beam, width, k, max_iters, _ptr(out_ids), _ptr(out_scores),
+        _ptr(out_iters), _ptr(status), _ptr(workspace), ws_bytes, _stream(stream)))

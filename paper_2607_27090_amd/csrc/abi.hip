@@ -85,6 +85,134 @@ bool fused_applies(int64_t n, int32_t d, int32_t nq, int64_t bank_stride, int32_
     return is::scan_mfma_applies(n, d, nq, bank_stride, dtype) && n > 2 * is::select_chunk_len();
 }
 
+// Enqueues the retrieval kernels (arguments already validated, workspace of
+// at least retrieve_need bytes).
+int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                     int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
+                     int32_t dtype, void* workspace, hipStream_t st) {
+    const RetrieveLayout lay = retrieve_layout(n, k, nq);
+    const bool fused = fused_applies(n, d, nq, bank_stride, dtype);
+    char* ws = (char*)workspace;
+    hipError_t e;
+    if (fused) {
+        // 1. dense scores of the first S rows; 2. their k winners, whose k-th
+        // key bounds the answer from below; 3. the rest of the bank keeps
+        // only keys above it; 4. exact ranking of sample winners + survivors
+        const FusedLayout fl = fused_layout(n, k, nq);
+        const int64_t S = fl.sample;
+        float* sc = (float*)(ws + fl.scores_off);
+        uint64_t* first = (uint64_t*)(ws + fl.first_off);
+        uint32_t* counts = (uint32_t*)(ws + fl.counts_off);
+        uint64_t* regions = (uint64_t*)(ws + fl.regions_off);
+        e = is::launch_scan_mfma(query_emb, bank, d, nq, 0, S, sc, S, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+        e = is::launch_select_scores(sc, S, k, nq, 1, first, nullptr, nullptr, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        e = is::launch_scan_mfma_filter(query_emb, bank, d, nq, S, n, first, k, regions, counts,
+                                        st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+        int G;
+        int64_t rpb;
+        is::mfma_grid(n - S, &G, &rpb);
+        e = is::launch_select_regions(first, regions, counts, G, rpb, k, nq, out_ids, out_scores,
+                                      st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        return ok();
+    }
+    float* scores = (float*)(ws + lay.scores_off);
+    e = is::scan_mfma_applies(n, d, nq, bank_stride, dtype)
+            ? is::launch_scan_mfma(query_emb, bank, d, nq, 0, n, scores, n, st)
+            : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
+    if (lay.nchunks == 1) {
+        e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        return ok();
+    }
+    uint64_t* a = (uint64_t*)(ws + lay.cand_a_off);
+    uint64_t* b = (uint64_t*)(ws + lay.cand_b_off);
+    e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, nullptr, nullptr, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+    int64_t M = (int64_t)lay.nchunks * k;
+    const int64_t chunk = is::select_chunk_len();
+    while (M > chunk) {
+        const int nch = (int)((M + chunk - 1) / chunk);
+        e = is::launch_select_keys(a, M, k, nq, nch, b, nullptr, nullptr, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        uint64_t* tmp = a;
+        a = b;
+        b = tmp;
+        M = (int64_t)nch * k;
+    }
+    e = is::launch_select_keys(a, M, k, nq, 1, nullptr, out_ids, out_scores, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+size_t retrieve_need(int64_t n, int32_t d, int32_t k, int32_t nq, int64_t bank_stride,
+                     int32_t dtype) {
+    return fused_applies(n, d, nq, bank_stride, dtype) ? fused_layout(n, k, nq).total
+                                                      : retrieve_layout(n, k, nq).total;
+}
+
+// Graph build: bank rows go through exact retrieval in batches of up to
+// kAnnBuildBatch queries (k = R + 1); then the forward lists, then the
+// reverse-edge buckets.
+constexpr int kAnnBuildBatch = 256;
+
+struct AnnBuildLayout {
+    int batch;
+    size_t ids_off, fwd_off, merge_off, total;
+};
+
+AnnBuildLayout ann_build_layout(int64_t n, int32_t d, int32_t R, int32_t dtype) {
+    AnnBuildLayout lay{};
+    lay.batch = (int)std::min<int64_t>(kAnnBuildBatch, n);
+    const int last = (int)(n - (n - 1) / lay.batch * lay.batch);
+    size_t off = round_up(std::max(retrieve_need(n, d, R + 1, lay.batch, 0, dtype),
+                                   retrieve_need(n, d, R + 1, last, 0, dtype)),
+                          256);
+    lay.ids_off = off;
+    off = round_up(off + (size_t)lay.batch * (R + 1) * sizeof(int32_t), 256);
+    lay.fwd_off = off;
+    off = round_up(off + (size_t)n * R * sizeof(int32_t), 256);
+    lay.merge_off = off;
+    off = round_up(off + is::ann_merge_scratch_bytes(n, R), 256);
+    lay.total = off;
+    return lay;
+}
+
+// Graph search: exact retrieval of the best min(beam, n_seeds) seeds, then
+// the beam search.
+struct AnnSearchLayout {
+    int n_init;
+    size_t ids_off, scores_off, total;
+};
+
+AnnSearchLayout ann_search_layout(int32_t n_seeds, int32_t d, int32_t beam, int32_t nq,
+                                  int32_t dtype) {
+    AnnSearchLayout lay{};
+    lay.n_init = std::min(beam, n_seeds);
+    size_t off = round_up(retrieve_need(n_seeds, d, lay.n_init, nq, 0, dtype), 256);
+    lay.ids_off = off;
+    off = round_up(off + (size_t)nq * lay.n_init * sizeof(int32_t), 256);
+    lay.scores_off = off;
+    off = round_up(off + (size_t)nq * lay.n_init * sizeof(float), 256);
+    lay.total = off;
+    return lay;
+}
+
+int check_ann_sizes(int64_t n, int32_t d, int32_t degree, int32_t dtype) {
+    if (n < 2 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [2, 2^31)", (long long)n);
+    if (d < 8 || d > 8192 || d % 8) return fail(IS_ERR_INVALID, "d=%d must be a multiple of 8 in [8, 8192]", d);
+    if (dtype != IS_DTYPE_F32 && dtype != IS_DTYPE_BF16)
+        return fail(IS_ERR_UNSUPPORTED, "dtype=%d is neither IS_DTYPE_F32 nor IS_DTYPE_BF16", dtype);
+    if (degree < 1 || degree > IS_ANN_MAX_DEGREE || degree > n - 1)
+        return fail(IS_ERR_INVALID, "degree=%d must be in [1, min(%d, n - 1)]", degree,
+                    IS_ANN_MAX_DEGREE);
+    return IS_OK;
+}
+
 // A pre-RoPE store pointer is usable by the inject kernel if it is memory of
 // the current device, managed memory, or pinned host memory mapped into the
 // device's address space at the same address.
@@ -182,70 +310,14 @@ int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, i
         return fail(IS_ERR_INVALID, "query_emb and bank must be 16-byte aligned");
     if (!aligned(out_ids, 4) || (out_scores && !aligned(out_scores, 4)))
         return fail(IS_ERR_INVALID, "out_ids/out_scores must be 4-byte aligned");
-    const RetrieveLayout lay = retrieve_layout(n, k, nq);
-    const bool fused = fused_applies(n, d, nq, bank_stride, dtype);
-    const size_t need = fused ? fused_layout(n, k, nq).total : lay.total;
+    const size_t need = retrieve_need(n, d, k, nq, bank_stride, dtype);
     if (!workspace || workspace_bytes < need)
         return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need,
                     workspace ? workspace_bytes : (size_t)0);
     if (!aligned(workspace, 256)) return fail(IS_ERR_INVALID, "workspace must be 256-byte aligned");
 
-    hipStream_t st = (hipStream_t)stream;
-    char* ws = (char*)workspace;
-    hipError_t e;
-    if (fused) {
-        // 1. dense scores of the first S rows; 2. their k winners, whose k-th
-        // key bounds the answer from below; 3. the rest of the bank keeps
-        // only keys above it; 4. exact ranking of sample winners + survivors
-        const FusedLayout fl = fused_layout(n, k, nq);
-        const int64_t S = fl.sample;
-        float* sc = (float*)(ws + fl.scores_off);
-        uint64_t* first = (uint64_t*)(ws + fl.first_off);
-        uint32_t* counts = (uint32_t*)(ws + fl.counts_off);
-        uint64_t* regions = (uint64_t*)(ws + fl.regions_off);
-        e = is::launch_scan_mfma(query_emb, bank, d, nq, 0, S, sc, S, st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
-        e = is::launch_select_scores(sc, S, k, nq, 1, first, nullptr, nullptr, st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-        e = is::launch_scan_mfma_filter(query_emb, bank, d, nq, S, n, first, k, regions, counts,
-                                        st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
-        int G;
-        int64_t rpb;
-        is::mfma_grid(n - S, &G, &rpb);
-        e = is::launch_select_regions(first, regions, counts, G, rpb, k, nq, out_ids, out_scores,
-                                      st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-        return ok();
-    }
-    float* scores = (float*)(ws + lay.scores_off);
-    e = is::scan_mfma_applies(n, d, nq, bank_stride, dtype)
-            ? is::launch_scan_mfma(query_emb, bank, d, nq, 0, n, scores, n, st)
-            : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
-    if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
-    if (lay.nchunks == 1) {
-        e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-        return ok();
-    }
-    uint64_t* a = (uint64_t*)(ws + lay.cand_a_off);
-    uint64_t* b = (uint64_t*)(ws + lay.cand_b_off);
-    e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, nullptr, nullptr, st);
-    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-    int64_t M = (int64_t)lay.nchunks * k;
-    const int64_t chunk = is::select_chunk_len();
-    while (M > chunk) {
-        const int nch = (int)((M + chunk - 1) / chunk);
-        e = is::launch_select_keys(a, M, k, nq, nch, b, nullptr, nullptr, st);
-        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-        uint64_t* tmp = a;
-        a = b;
-        b = tmp;
-        M = (int64_t)nch * k;
-    }
-    e = is::launch_select_keys(a, M, k, nq, 1, nullptr, out_ids, out_scores, st);
-    if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
-    return ok();
+    return enqueue_retrieve(query_emb, bank, n, d, k, out_ids, out_scores, nq, bank_stride, dtype,
+                            workspace, (hipStream_t)stream);
 }
 
 int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
@@ -370,6 +442,128 @@ int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int
                                            max_blocks, max_tokens, rope_theta, inv_freq, pairing,
                                            status, (hipStream_t)stream);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "paged scores launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
+int is_ann_build_workspace_size(int64_t n, int32_t d, int32_t degree, int32_t dtype,
+                                size_t* bytes) {
+    if (!bytes) return fail(IS_ERR_INVALID, "bytes is NULL");
+    *bytes = 0;
+    const int rc = check_ann_sizes(n, d, degree, dtype);
+    if (rc) return rc;
+    *bytes = ann_build_layout(n, d, degree, dtype).total;
+    return ok();
+}
+
+int is_ann_build(const void* bank, int64_t n, int32_t d, int32_t degree, int32_t dtype,
+                 int32_t n_seeds, int32_t* graph, int32_t* fwd, int32_t* seed_ids,
+                 void* seed_bank, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!bank || !graph) return fail(IS_ERR_INVALID, "bank and graph must be non-NULL");
+    int rc = check_ann_sizes(n, d, degree, dtype);
+    if (rc) return rc;
+    if (n_seeds < 0 || n_seeds > n)
+        return fail(IS_ERR_INVALID, "n_seeds=%d must be in [0, n]", n_seeds);
+    if (n_seeds > 0 && (!seed_ids || !seed_bank))
+        return fail(IS_ERR_INVALID, "seed_ids and seed_bank must be non-NULL when n_seeds > 0");
+    if (!aligned(bank, 16) || (seed_bank && !aligned(seed_bank, 16)))
+        return fail(IS_ERR_INVALID, "bank and seed_bank must be 16-byte aligned");
+    if (!aligned(graph, 4) || (fwd && !aligned(fwd, 4)) || (seed_ids && !aligned(seed_ids, 4)))
+        return fail(IS_ERR_INVALID, "graph, fwd and seed_ids must be 4-byte aligned");
+    const AnnBuildLayout lay = ann_build_layout(n, d, degree, dtype);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(IS_ERR_INVALID, "workspace must be 256-byte aligned");
+
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    int32_t* ids = (int32_t*)(ws + lay.ids_off);
+    int32_t* F = fwd ? fwd : (int32_t*)(ws + lay.fwd_off);
+    const size_t esize = dtype == IS_DTYPE_F32 ? 4 : 2;
+    for (int64_t row0 = 0; row0 < n; row0 += lay.batch) {
+        const int nb = (int)std::min<int64_t>(lay.batch, n - row0);
+        const void* rows = (const char*)bank + (size_t)row0 * d * esize;
+        rc = enqueue_retrieve(rows, bank, n, d, degree + 1, ids, nullptr, nb, 0, dtype, ws, st);
+        if (rc) return rc;
+        hipError_t e = is::launch_ann_take(ids, row0, nb, degree, F, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "graph build launch: %s", hipGetErrorString(e));
+    }
+    hipError_t e = is::launch_ann_merge(F, n, degree, ws + lay.merge_off, graph, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "graph merge launch: %s", hipGetErrorString(e));
+    if (n_seeds > 0) {
+        e = is::launch_ann_seeds(bank, n, d, dtype, n_seeds, seed_ids, seed_bank, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "seed launch: %s", hipGetErrorString(e));
+    }
+    return ok();
+}
+
+static int check_ann_search_sizes(int32_t nq, int64_t n, int32_t d, int32_t dtype, int32_t degree,
+                                  int32_t n_seeds, int32_t beam, int32_t width, int32_t k,
+                                  int32_t max_iters) {
+    int rc = check_ann_sizes(n, d, degree, dtype);
+    if (rc) return rc;
+    if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
+    const int64_t row_chunks = (int64_t)d * (dtype == IS_DTYPE_F32 ? 4 : 2) / 16;
+    if (row_chunks > is::ann_max_row_chunks())
+        return fail(IS_ERR_UNSUPPORTED, "rows of %lld bytes exceed the search limit of %d bytes",
+                    (long long)row_chunks * 16, is::ann_max_row_chunks() * 16);
+    if (n_seeds < 1 || n_seeds > n)
+        return fail(IS_ERR_INVALID, "n_seeds=%d must be in [1, n]", n_seeds);
+    if (beam < 1 || beam > IS_ANN_MAX_BEAM)
+        return fail(IS_ERR_INVALID, "beam=%d must be in [1, %d]", beam, IS_ANN_MAX_BEAM);
+    if (width < 1 || width > IS_ANN_MAX_WIDTH || width * degree > IS_ANN_MAX_EXPAND)
+        return fail(IS_ERR_INVALID, "width=%d must be in [1, %d] with width*degree <= %d", width,
+                    IS_ANN_MAX_WIDTH, IS_ANN_MAX_EXPAND);
+    if (k < 1 || k > beam) return fail(IS_ERR_INVALID, "k=%d must be in [1, beam=%d]", k, beam);
+    if (max_iters < 0) return fail(IS_ERR_INVALID, "max_iters=%d must be >= 0", max_iters);
+    return IS_OK;
+}
+
+int is_ann_search_workspace_size(int32_t n_seeds, int32_t d, int32_t beam, int32_t nq,
+                                 int32_t dtype, size_t* bytes) {
+    if (!bytes) return fail(IS_ERR_INVALID, "bytes is NULL");
+    *bytes = 0;
+    if (n_seeds < 1 || beam < 1 || beam > IS_ANN_MAX_BEAM || nq < 1 || nq > 65535)
+        return fail(IS_ERR_INVALID, "n_seeds, beam and nq out of range");
+    const int rc = check_retrieve_sizes(n_seeds, d, std::min(beam, n_seeds), nq, dtype);
+    if (rc) return rc;
+    *bytes = ann_search_layout(n_seeds, d, beam, nq, dtype).total;
+    return ok();
+}
+
+int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n, int32_t d,
+                  int32_t dtype, const int32_t* graph, int32_t degree, const int32_t* seed_ids,
+                  const void* seed_bank, int32_t n_seeds, int32_t beam, int32_t width, int32_t k,
+                  int32_t max_iters, int32_t* out_ids, float* out_scores, int32_t* out_iters,
+                  uint32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!query_emb || !bank || !graph || !seed_ids || !seed_bank || !out_ids)
+        return fail(IS_ERR_INVALID,
+                    "query_emb, bank, graph, seed_ids, seed_bank and out_ids must be non-NULL");
+    int rc = check_ann_search_sizes(nq, n, d, dtype, degree, n_seeds, beam, width, k, max_iters);
+    if (rc) return rc;
+    if (!aligned(query_emb, 16) || !aligned(bank, 16) || !aligned(seed_bank, 16))
+        return fail(IS_ERR_INVALID, "query_emb, bank and seed_bank must be 16-byte aligned");
+    if (!aligned(graph, 4) || !aligned(seed_ids, 4) || !aligned(out_ids, 4) ||
+        (out_scores && !aligned(out_scores, 4)) || (out_iters && !aligned(out_iters, 4)) ||
+        (status && !aligned(status, 4)))
+        return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    const AnnSearchLayout lay = ann_search_layout(n_seeds, d, beam, nq, dtype);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(IS_ERR_INVALID, "workspace must be 256-byte aligned");
+
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    int32_t* init_ids = (int32_t*)(ws + lay.ids_off);
+    float* init_scores = (float*)(ws + lay.scores_off);
+    rc = enqueue_retrieve(query_emb, seed_bank, n_seeds, d, lay.n_init, init_ids, init_scores, nq,
+                          0, dtype, ws, st);
+    if (rc) return rc;
+    hipError_t e = is::launch_ann_search(query_emb, nq, bank, n, d, dtype, graph, degree, seed_ids,
+                                         n_seeds, init_ids, init_scores, lay.n_init, beam, width,
+                                         k, max_iters, out_ids, out_scores, out_iters, status, st);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "graph search launch: %s", hipGetErrorString(e));
     return ok();
 }
 

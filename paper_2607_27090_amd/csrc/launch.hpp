@@ -67,4 +67,20 @@ hipError_t launch_paged_scores(const void* q, const int32_t* qpos, const void* p
                                const double* inv_freq, int32_t interleaved, uint32_t* status,
                                hipStream_t st);
 
+// ann.hip
+hipError_t launch_ann_take(const int32_t* ids, int64_t row0, int nb, int R, int32_t* F,
+                           hipStream_t st);
+size_t ann_merge_scratch_bytes(int64_t n, int R);
+hipError_t launch_ann_merge(const int32_t* F, int64_t n, int R, void* scratch, int32_t* G,
+                            hipStream_t st);
+hipError_t launch_ann_seeds(const void* bank, int64_t n, int d, int dtype, int n_seeds,
+                            int32_t* seed_ids, void* seed_bank, hipStream_t st);
+int ann_max_row_chunks();
+hipError_t launch_ann_search(const void* query, int nq, const void* bank, int64_t n, int d,
+                             int dtype, const int32_t* graph, int R, const int32_t* seed_ids,
+                             int n_seeds, const int32_t* init_local, const float* init_score,
+                             int n_init, int B, int P, int k, int max_iters, int32_t* out_ids,
+                             float* out_scores, int32_t* out_iters, uint32_t* status,
+                             hipStream_t st);
+
 }  // namespace is

@@ -14,36 +14,12 @@
 //     digits from the highest differing bit). Chunks emit k candidates each;
 //     a final pass over the candidates orders the winners (score desc,
 //     id asc).
-#include "common.hpp"
+#include "wave.hpp"
 #include "launch.hpp"
 
 namespace is {
 
 // ---- scan ------------------------------------------------------------------
-
-struct F32Tag {};
-struct BF16Tag {};
-
-__device__ __forceinline__ float dot16(uint4 a, uint4 b, F32Tag) {
-    float s = __uint_as_float(a.x) * __uint_as_float(b.x);
-    s = fmaf(__uint_as_float(a.y), __uint_as_float(b.y), s);
-    s = fmaf(__uint_as_float(a.z), __uint_as_float(b.z), s);
-    s = fmaf(__uint_as_float(a.w), __uint_as_float(b.w), s);
-    return s;
-}
-
-__device__ __forceinline__ float dot16(uint4 a, uint4 b, BF16Tag) {
-    // bf16 x bf16 products are exact in fp32
-    float s = bf16_lo(a.x) * bf16_lo(b.x);
-    s = fmaf(bf16_hi(a.x), bf16_hi(b.x), s);
-    s = fmaf(bf16_lo(a.y), bf16_lo(b.y), s);
-    s = fmaf(bf16_hi(a.y), bf16_hi(b.y), s);
-    s = fmaf(bf16_lo(a.z), bf16_lo(b.z), s);
-    s = fmaf(bf16_hi(a.z), bf16_hi(b.z), s);
-    s = fmaf(bf16_lo(a.w), bf16_lo(b.w), s);
-    s = fmaf(bf16_hi(a.w), bf16_hi(b.w), s);
-    return s;
-}
 
 // Reduce V partial sums held by every lane of a wave. On return the lane
 // holds the full sum of value index `*which`; lanes whose low (6 - log2 V)
@@ -501,12 +477,6 @@ struct SelShared {
     uint32_t above;
 };
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int off) {
-    const uint32_t lo = __shfl_xor((uint32_t)v, off, kWave);
-    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), off, kWave);
-    return ((uint64_t)hi << 32) | lo;
-}
-
 __device__ __forceinline__ uint64_t wave_min64(uint64_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -520,12 +490,6 @@ __device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v |= shfl_xor64(v, off);
     return v;
-}
-
-// Lanes below this one whose bit is set in a wave-wide mask.
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
-    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
 // One block selects the `want` = min(k, valid keys) largest keys held in its

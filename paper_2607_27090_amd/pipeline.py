@@ -5,8 +5,9 @@ from __future__ import annotations
 
 import torch
 
-from . import (IS_DTYPE_BF16, IS_DTYPE_F32, IS_ROPE_HALF_SPLIT, is_inject, is_inject_rotary,
-               is_retrieve, is_retrieve_workspace_size, is_slot_map)
+from . import (IS_DTYPE_BF16, IS_DTYPE_F32, IS_ROPE_HALF_SPLIT, is_ann_build,
+               is_ann_build_workspace_size, is_ann_search, is_ann_search_workspace_size,
+               is_inject, is_inject_rotary, is_retrieve, is_retrieve_workspace_size, is_slot_map)
 
 
 class RequestBuffers:
@@ -78,3 +79,41 @@ def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, p
                fact_offsets=store["fact_offsets"], fact_lens=store["fact_lens"],
                lens_stride=lens_stride, reverse_rank=reverse_rank, inv_freq=inv_freq,
                pairing=pairing, stream=stream)
+
+
+class AnnIndex:
+    """Proximity graph of one bank with the search's seeds (built on the
+    device by is_ann_build), and cached search workspaces."""
+
+    def __init__(self, bank: torch.Tensor, *, degree: int = 64, n_seeds: int = 1024,
+                 keep_forward: bool = False, stream=None):
+        n, d = bank.shape
+        dev = bank.device
+        self.bank, self.n, self.d, self.degree = bank, n, d, degree
+        self.dtype = IS_DTYPE_F32 if bank.dtype == torch.float32 else IS_DTYPE_BF16
+        self.n_seeds = min(n_seeds, n)
+        self.graph = torch.empty(n, degree, dtype=torch.int32, device=dev)
+        self.fwd = torch.empty(n, degree, dtype=torch.int32, device=dev) if keep_forward else None
+        self.seed_ids = torch.empty(self.n_seeds, dtype=torch.int32, device=dev)
+        self.seed_bank = torch.empty(self.n_seeds, d, dtype=bank.dtype, device=dev)
+        ws = torch.empty(is_ann_build_workspace_size(n, d, degree, self.dtype), dtype=torch.uint8,
+                         device=dev)
+        is_ann_build(bank, n, d, degree, self.graph, n_seeds=self.n_seeds, fwd=self.fwd,
+                     seed_ids=self.seed_ids, seed_bank=self.seed_bank, workspace=ws,
+                     stream=stream)
+        self._ws = {}
+
+    def workspace(self, nq: int, beam: int) -> torch.Tensor:
+        key = (nq, beam)
+        if key not in self._ws:
+            size = is_ann_search_workspace_size(self.n_seeds, self.d, beam, nq, self.dtype)
+            self._ws[key] = torch.empty(max(size, 256), dtype=torch.uint8, device=self.bank.device)
+        return self._ws[key]
+
+    def search(self, query, out_ids, *, nq: int, k: int, beam: int = 64, width: int = 1,
+               max_iters: int = 256, out_scores=None, out_iters=None, status=None, stream=None):
+        is_ann_search(query, self.bank, self.n, self.d, self.graph, self.degree, self.seed_ids,
+                      self.seed_bank, out_ids, nq=nq, n_seeds=self.n_seeds, beam=beam,
+                      width=width, k=k, max_iters=max_iters, out_scores=out_scores,
+                      out_iters=out_iters, status=status, workspace=self.workspace(nq, beam),
+                      stream=stream)

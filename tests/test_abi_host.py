@@ -171,3 +171,65 @@ def _scores(**kw):
 ])
 def test_paged_scores_rejects(kw, code):
     assert _scores(**kw) == code
+
+
+def _ann_build(**kw):
+    a = dict(bank=A, n=1000, d=64, R=16, dt=1, ns=8, G=A, F=None, sid=A, sb=A, ws=A,
+             wsb=1 << 34)
+    a.update(kw)
+    return isl.load_library().is_ann_build(a["bank"], a["n"], a["d"], a["R"], a["dt"], a["ns"],
+                                           a["G"], a["F"], a["sid"], a["sb"], a["ws"], a["wsb"],
+                                           None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bank=None), isl.IS_ERR_INVALID), (dict(G=None), isl.IS_ERR_INVALID),
+    (dict(n=1), isl.IS_ERR_INVALID), (dict(d=12), isl.IS_ERR_INVALID),
+    (dict(d=8200), isl.IS_ERR_INVALID), (dict(dt=3), isl.IS_ERR_UNSUPPORTED),
+    (dict(R=0), isl.IS_ERR_INVALID), (dict(R=129), isl.IS_ERR_INVALID),
+    (dict(n=10, R=10), isl.IS_ERR_INVALID), (dict(ns=-1), isl.IS_ERR_INVALID),
+    (dict(ns=1001), isl.IS_ERR_INVALID), (dict(sid=None), isl.IS_ERR_INVALID),
+    (dict(sb=None), isl.IS_ERR_INVALID), (dict(bank=A + 8), isl.IS_ERR_INVALID),
+    (dict(G=A + 2), isl.IS_ERR_INVALID), (dict(ws=None), isl.IS_ERR_WORKSPACE),
+    (dict(wsb=1024), isl.IS_ERR_WORKSPACE), (dict(ws=A + 64), isl.IS_ERR_INVALID),
+])
+def test_ann_build_rejects(kw, code):
+    assert _ann_build(**kw) == code
+    assert isl.load_library().is_last_error().decode()
+
+
+def _ann_search(**kw):
+    a = dict(q=A, nq=4, bank=A, n=1000, d=64, dt=1, G=A, R=16, sid=A, sb=A, ns=8, B=64, P=1,
+             k=10, T=100, ids=A, sc=None, it=None, st=None, ws=A, wsb=1 << 34)
+    a.update(kw)
+    return isl.load_library().is_ann_search(
+        a["q"], a["nq"], a["bank"], a["n"], a["d"], a["dt"], a["G"], a["R"], a["sid"], a["sb"],
+        a["ns"], a["B"], a["P"], a["k"], a["T"], a["ids"], a["sc"], a["it"], a["st"], a["ws"],
+        a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), isl.IS_ERR_INVALID), (dict(G=None), isl.IS_ERR_INVALID),
+    (dict(sid=None), isl.IS_ERR_INVALID), (dict(sb=None), isl.IS_ERR_INVALID),
+    (dict(ids=None), isl.IS_ERR_INVALID), (dict(nq=0), isl.IS_ERR_INVALID),
+    (dict(nq=65536), isl.IS_ERR_INVALID), (dict(d=4104), isl.IS_ERR_UNSUPPORTED),
+    (dict(dt=0, d=2056), isl.IS_ERR_UNSUPPORTED), (dict(R=129), isl.IS_ERR_INVALID),
+    (dict(ns=0), isl.IS_ERR_INVALID), (dict(ns=1001), isl.IS_ERR_INVALID),
+    (dict(B=0), isl.IS_ERR_INVALID), (dict(B=257), isl.IS_ERR_INVALID),
+    (dict(P=0), isl.IS_ERR_INVALID), (dict(P=5), isl.IS_ERR_INVALID),
+    (dict(P=3, R=100), isl.IS_ERR_INVALID), (dict(k=0), isl.IS_ERR_INVALID),
+    (dict(k=65), isl.IS_ERR_INVALID), (dict(T=-1), isl.IS_ERR_INVALID),
+    (dict(q=A + 4), isl.IS_ERR_INVALID), (dict(sb=A + 8), isl.IS_ERR_INVALID),
+    (dict(it=A + 2), isl.IS_ERR_INVALID), (dict(ws=None), isl.IS_ERR_WORKSPACE),
+    (dict(wsb=512), isl.IS_ERR_WORKSPACE),
+])
+def test_ann_search_rejects(kw, code):
+    assert _ann_search(**kw) == code
+    assert isl.load_library().is_last_error().decode()
+
+
+def test_ann_workspace_sizes_are_pure_host():
+    assert isl.is_ann_build_workspace_size(1000000, 1024, 64, isl.IS_DTYPE_BF16) > 1000000 * 64 * 4
+    assert isl.is_ann_search_workspace_size(1024, 1024, 64, 256, isl.IS_DTYPE_BF16) >= 256 * 64 * 8
+    with pytest.raises(isl.InferScaleError):
+        isl.is_ann_build_workspace_size(10, 64, 10, isl.IS_DTYPE_F32)

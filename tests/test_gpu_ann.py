@@ -1,0 +1,197 @@
+"""GPU parity of the graph-ANN backend (is_ann_build, is_ann_search) against
+the oracle in oracle/ann.c.
+
+Bit-exact cases use small-integer embeddings: every product and partial sum
+is an integer below 2^24, so the kernels' fp32 scores equal the oracle's
+binary64 ones exactly and every decision (neighbour lists, ties to the lower
+id, which entry is expanded next) is taken identically on both sides. On
+real-valued embeddings the neighbour lists may differ only at near ties
+(scores closer than 1e-6), and the final lists must be exactly the oracle's
+merge of the GPU's own forward lists.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from paper_2607_27090_amd import IS_DEV_ID_RANGE, is_ann_search, is_ann_search_workspace_size
+from paper_2607_27090_amd.pipeline import AnnIndex
+from tests import parity
+from tests.gpu_harness import host_emb, log
+
+pytestmark = pytest.mark.gpu
+
+
+def int_bank(seed, n, d, dtype, lo=-2, hi=2):
+    rng = np.random.default_rng(seed)
+    x = rng.integers(lo, hi + 1, size=(n, d)).astype(np.float32)
+    t = torch.from_numpy(x).cuda()
+    return t if dtype == "f32" else t.to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("dtype,n,d,R,ns", [
+    ("f32", 3000, 136, 64, 100),   # 12 retrieval batches, the last one ragged
+    ("bf16", 3000, 128, 64, 64),   # matrix-core scan for the forward lists
+    ("bf16", 700, 40, 7, 7),       # odd degree, row-scan path
+    ("f32", 530, 64, 1, 1),        # degree 1: no forward half, one fill
+    ("bf16", 300, 8, 128, 300),    # the largest degree, every row a seed
+    ("f32", 129, 16, 128, 5),      # degree = n - 1: complete graph
+])
+def test_build_integer_bank_bit_exact(dtype, n, d, R, ns):
+    log(f"ann build {dtype} n={n} d={d} R={R}")
+    bank = int_bank(n + d + R, n, d, dtype)
+    idx = AnnIndex(bank, degree=R, n_seeds=ns, keep_forward=True)
+    torch.cuda.synchronize()
+    X, odt = host_emb(bank)
+    F, G = oracle.ann_build(X, n, d, R, odt)
+    assert np.array_equal(idx.fwd.cpu().numpy(), F)
+    assert np.array_equal(idx.graph.cpu().numpy(), G)
+    want = (np.arange(ns, dtype=np.int64) * n // ns).astype(np.int32)
+    assert np.array_equal(idx.seed_ids.cpu().numpy(), want)
+    assert torch.equal(idx.seed_bank, bank[torch.from_numpy(want).long().cuda()])
+
+
+def test_build_clustered_bank_near_ties_only():
+    w = workloads.RETRIEVAL1M.with_(n=2500, d_e=256, index=40)
+    bank = workloads.make_bank(w, "cuda")
+    R = 64
+    log("ann build clustered bf16 n=2500 d=256")
+    idx = AnnIndex(bank, degree=R, n_seeds=64, keep_forward=True)
+    torch.cuda.synchronize()
+    X, odt = host_emb(bank)
+    F_o = oracle.ann_knn(X, w.n, w.d_e, R, odt)
+    F_g = idx.fwd.cpu().numpy()
+    S = oracle.scores(X, X, w.n, w.d_e, w.n, 0, odt)
+    np.fill_diagonal(S, -np.inf)
+    swaps = sum(parity.check_ids(F_g[i], F_o[i], S[i], w.n) for i in range(w.n))
+    assert swaps <= w.n * R // 1000
+    assert np.array_equal(idx.graph.cpu().numpy(), oracle.ann_merge(F_g))
+
+
+def random_graph(seed, n, R):
+    rng = np.random.default_rng(seed)
+    G = np.empty((n, R), dtype=np.int32)
+    for i in range(n):
+        c = rng.choice(n - 1, size=R, replace=False)
+        G[i] = np.where(c >= i, c + 1, c)
+    return G
+
+
+def run_search(bank, graph, seeds, query, *, beam, width, k, max_iters, status=None):
+    n, d = bank.shape
+    nq = query.shape[0]
+    R = graph.shape[1]
+    g = torch.from_numpy(graph).cuda()
+    s = torch.from_numpy(seeds).cuda()
+    sb = bank[s.long()].contiguous()
+    ids = torch.full((nq, k), -7, dtype=torch.int32, device="cuda")
+    sc = torch.empty(nq, k, dtype=torch.float32, device="cuda")
+    it = torch.empty(nq, dtype=torch.int32, device="cuda")
+    dt = 0 if bank.dtype == torch.float32 else 1
+    ws = torch.empty(max(256, is_ann_search_workspace_size(len(seeds), d, beam, nq, dt)),
+                     dtype=torch.uint8, device="cuda")
+    is_ann_search(query, bank, n, d, g, R, s, sb, ids, nq=nq, n_seeds=len(seeds), beam=beam,
+                  width=width, k=k, max_iters=max_iters, out_scores=sc, out_iters=it,
+                  status=status, workspace=ws)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), sc.cpu().numpy(), it.cpu().numpy()
+
+
+def check_search(bank, graph, seeds, query, **kw):
+    ids, sc, it = run_search(bank, graph, seeds, query, **kw)
+    X, odt = host_emb(bank)
+    Q, _ = host_emb(query)
+    r = oracle.ann_search(Q, X, bank.shape[0], bank.shape[1], graph, seeds, kw["beam"], kw["k"],
+                          kw["max_iters"], width=kw["width"], dtype=odt)
+    assert np.array_equal(ids, r["ids"])
+    assert np.array_equal(sc.astype(np.float64), r["scores"])
+    assert np.array_equal(it, r["iters"])
+    return it
+
+
+@pytest.mark.parametrize("dtype,n,d,R,ns,beam,width,k,max_iters,nq", [
+    ("f32", 2000, 64, 16, 64, 64, 1, 10, 300, 24),
+    ("bf16", 2000, 64, 16, 64, 64, 4, 64, 300, 24),     # k = beam, widest expansion
+    ("f32", 2000, 64, 16, 64, 1, 1, 1, 50, 8),          # beam 1: hill climbing
+    ("bf16", 2000, 136, 32, 300, 256, 2, 100, 1000, 6),  # the largest beam; ragged rows
+    ("f32", 2000, 64, 16, 40, 32, 1, 32, 0, 5),         # no iterations: the best seeds
+    ("bf16", 900, 8, 8, 1, 16, 3, 5, 200, 3),           # one seed; 16-byte rows
+    ("f32", 600, 2048, 8, 20, 64, 2, 20, 100, 2),       # 8 KiB fp32 rows
+    ("bf16", 600, 4096, 8, 20, 64, 2, 20, 100, 2),      # 8 KiB bf16 rows
+    ("f32", 2000, 64, 16, 64, 64, 1, 10, 7, 4),         # stopped by max_iters
+])
+def test_search_integer_bank_bit_exact(dtype, n, d, R, ns, beam, width, k, max_iters, nq):
+    log(f"ann search {dtype} n={n} d={d} R={R} beam={beam} width={width} k={k}")
+    bank = int_bank(n * 7 + d, n, d, dtype)
+    query = int_bank(n * 7 + d + 1, nq, d, dtype)
+    seeds = (np.arange(ns, dtype=np.int64) * n // ns).astype(np.int32)
+    X, odt = host_emb(bank)
+    # the oracle's own graph where it is cheap to build, else a random one
+    small = R <= 16 and d <= 512
+    graph = oracle.ann_build(X, n, d, R, odt)[1] if small else random_graph(n + R, n, R)
+    check_search(bank, graph, seeds, query, beam=beam, width=width, k=k, max_iters=max_iters)
+
+
+def test_search_visited_table_refills():
+    # a random degree-64 graph and a 256-wide beam score thousands of facts
+    # per query: the visited table passes half full and is refilled with the
+    # beam several times, which must not change the result
+    n, d, R = 20000, 16, 64
+    bank = int_bank(11, n, d, "bf16", -4, 4)
+    query = int_bank(12, 4, d, "bf16", -4, 4)
+    seeds = (np.arange(256, dtype=np.int64) * n // 256).astype(np.int32)
+    log("ann search table refill")
+    it = check_search(bank, random_graph(13, n, R), seeds, query, beam=256, width=4, k=50,
+                      max_iters=400)
+    # at least 32 iterations of 256 neighbours each: several times what the
+    # table holds before it is refilled
+    assert (it >= 32).all()
+
+
+def test_search_bad_graph_entries_flagged_and_skipped():
+    n, d, R = 500, 32, 8
+    bank = int_bank(21, n, d, "f32")
+    query = int_bank(22, 3, d, "f32")
+    graph = random_graph(23, n, R)
+    graph[::7, 3] = n           # past the end
+    graph[::11, 5] = -1         # negative
+    seeds = np.arange(0, n, 25, dtype=np.int32)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    log("ann search bad graph entries")
+    check_search(bank, graph, seeds, query, beam=32, width=2, k=16, max_iters=100, status=status)
+    assert int(status.item()) & IS_DEV_ID_RANGE
+
+
+def test_search_clustered_bank_matches_oracle_and_recalls():
+    w = workloads.RETRIEVAL1M.with_(n=20000, d_e=256, nq=32, index=41)
+    bank = workloads.make_bank(w, "cuda")
+    query = workloads.make_queries(w, "cuda")
+    log("ann clustered n=20000: build")
+    idx = AnnIndex(bank, degree=64, n_seeds=1024)
+    k = 50
+    ids = torch.empty(w.nq, k, dtype=torch.int32, device="cuda")
+    sc = torch.empty(w.nq, k, dtype=torch.float32, device="cuda")
+    it = torch.empty(w.nq, dtype=torch.int32, device="cuda")
+    log("ann clustered n=20000: search")
+    idx.search(query, ids, nq=w.nq, k=k, beam=64, width=1, max_iters=256, out_scores=sc,
+               out_iters=it)
+    torch.cuda.synchronize()
+    X, odt = host_emb(bank)
+    Q, _ = host_emb(query)
+    r = oracle.ann_search(Q, X, w.n, w.d_e, idx.graph.cpu().numpy(), idx.seed_ids.cpu().numpy(),
+                          64, k, 256, width=1, dtype=odt)
+    g_ids = ids.cpu().numpy()
+    S = oracle.scores(Q, X, w.n, w.d_e, w.nq, 0, odt)
+    same = 0
+    for q in range(w.nq):
+        # valid: distinct, ordered, scores within fp32 accumulation of exact
+        assert len(set(g_ids[q].tolist())) == k
+        parity.check_scores(sc.cpu().numpy()[q], S[q, g_ids[q]],
+                            np.abs(Q[q].astype(np.float64)).sum() * np.ones(k))
+        same += int(np.array_equal(g_ids[q], r["ids"][q]))
+    assert same >= w.nq - 2  # the walks diverge only where fp32 reorders a near tie
+    ex_ids, _ = oracle.topk(S, k)
+    recall = np.mean([len(set(g_ids[q]) & set(ex_ids[q])) / k for q in range(w.nq)])
+    log(f"ann clustered n=20000 recall@{k} {recall:.3f} iters {it.float().mean().item():.1f}")
+    assert recall >= 0.9
