@@ -294,9 +294,46 @@ __device__ __forceinline__ int block_compact(bool flag, SearchShared& sh, int* t
     return before + (int)lanes_below(m);
 }
 
+// Sum over the 16 lanes of a DPP row (lanes 16r .. 16r + 15); every lane of
+// the row receives the same sum: pairs, quads (quad_perm), then the two
+// quads of each half (row_half_mirror) and the two halves (row_mirror).
+__device__ __forceinline__ float row16_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+// 16-byte dot product of a query chunk and a row chunk. bf16: four packed
+// v_dot2c_f32_bf16 steps (exact products; each step adds two of them to
+// the running fp32 sum, rounding to nearest even with at most about one
+// ulp of error); fp32: a chain of fused multiply-adds.
+__device__ __forceinline__ float dot16q(uint4 q, uint4 r, F32Tag) { return dot16(q, r, F32Tag{}); }
+__device__ __forceinline__ float dot16q(uint4 q, uint4 r, BF16Tag) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    float s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q.x),
+                                              __builtin_bit_cast(bf16x2, r.x), 0.f, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q.y),
+                                        __builtin_bit_cast(bf16x2, r.y), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q.z),
+                                        __builtin_bit_cast(bf16x2, r.z), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q.w),
+                                        __builtin_bit_cast(bf16x2, r.w), s, false);
+    return s;
+}
+
+template <bool QREG, int E, int N>
+__device__ __forceinline__ uint4 qchunk(const SearchShared& sh, const uint4 (&qreg)[N],
+                                        const int (&chunk)[E], int e) {
+    if constexpr (QREG) return qreg[e];
+    else return sh.q[chunk[e]];
+}
+
 // E: 16-byte chunks per lane and row (a power of two); a row has
 // row_chunks <= 16 E chunks. NR rows per row group are loaded together.
-template <typename Tag, int E>
+// Rows of up to 2 KiB keep the lane's query chunks in registers.
+template <typename Tag, int E, bool QREG = (E <= 8)>
 __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
     const uint4* __restrict__ query, const uint4* __restrict__ bank, int64_t n, int row_chunks,
     const int32_t* __restrict__ graph, int R, const int32_t* __restrict__ seed_ids,
@@ -314,6 +351,18 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
     for (int s = t; s < kHashSize; s += kSrchThreads) sh.hash[s] = -1;
     if (t == 0) sh.flags = 0;
     __syncthreads();
+    // this lane's chunks of every row (chunks past the row's end re-read
+    // chunk 0 and count for nothing) and, for short rows, its query chunks
+    int chunk[E];
+    bool lane_ok[E];
+    uint4 qreg[QREG ? E : 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int ch = gl + e * kRowLanes;
+        lane_ok[e] = ch < row_chunks;
+        chunk[e] = lane_ok[e] ? ch : 0;
+        if constexpr (QREG) qreg[e] = sh.q[chunk[e]];
+    }
 
     // ---- the beam starts as the best seeds (re-ranked by global id) ----
     uint64_t ikey = 0;
@@ -381,31 +430,31 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
         if (t == 0) sh.hcount += C;
         __syncthreads();
 
-        // ---- C. scores: row group g takes rows g, g + 16, ... ----
+        // ---- C. scores: row group g takes rows g, g + 16, ... Every
+        // load of the round is issued before the first product; slots past
+        // the last candidate load nothing ----
         for (int r0 = g; r0 < C; r0 += kRowGroups * NR) {
             uint4 v[NR][E];
 #pragma unroll
             for (int r = 0; r < NR; ++r) {
                 const int c = r0 + r * kRowGroups;
-                const int64_t row = sh.cand_id[c < C ? c : r0];
-                const uint4* src = bank + row * row_chunks;
+                if (c < C) {
+                    const uint4* src = bank + (int64_t)sh.cand_id[c] * row_chunks;
 #pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const int ch = gl + e * kRowLanes;
-                    v[r][e] = src[ch < row_chunks ? ch : 0];
+                    for (int e = 0; e < E; ++e) v[r][e] = src[chunk[e]];
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int r = 0; r < NR; ++r) {
+                const int c = r0 + r * kRowGroups;
                 float s = 0.f;
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
-                    const int ch = gl + e * kRowLanes;
-                    if (ch < row_chunks) s += dot16(sh.q[ch], v[r][e], Tag{});
+                    const float t_e = dot16q(qchunk<QREG>(sh, qreg, chunk, e), v[r][e], Tag{});
+                    s += lane_ok[e] ? t_e : 0.f;
                 }
-#pragma unroll
-                for (int o = 1; o < kRowLanes; o <<= 1) s += __shfl_xor(s, o, kWave);
-                const int c = r0 + r * kRowGroups;
+                s = row16_sum(s);
                 if (gl == 0 && c < C) sh.cand_key[c] = rank_key(s, (uint32_t)sh.cand_id[c]);
             }
         }
