@@ -64,6 +64,15 @@ def parse():
     ap.add_argument("--consumer", action="store_true",
                     help="also time is_paged_scores (attention logits of a query after the "
                          "memory, 4 query heads per KV head) over every layer of each request")
+    ap.add_argument("--retriever", default="exact", choices=["exact", "ann"],
+                    help="exact top-k (is_retrieve), or the graph-ANN backend (is_ann_build "
+                         "once, untimed; is_ann_search per step)")
+    ap.add_argument("--beam", type=int, default=None,
+                    help="ANN beam width (default: the smallest of 64/128/256 that holds k)")
+    ap.add_argument("--width", type=int, default=4, help="ANN beam entries expanded per iteration")
+    ap.add_argument("--degree", type=int, default=64, help="ANN graph out-degree")
+    ap.add_argument("--seeds", type=int, default=1024, help="ANN search entry points")
+    ap.add_argument("--max-iters", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -80,7 +89,7 @@ def main():
     import workloads
     from paper_2607_27090_amd import (IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED, is_inject,
                                       is_inject_rotary, is_paged_scores, is_slot_map)
-    from paper_2607_27090_amd.pipeline import RequestBuffers
+    from paper_2607_27090_amd.pipeline import AnnIndex, RequestBuffers
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda"
@@ -111,6 +120,30 @@ def main():
     bufs = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
                            max_tokens=w.max_tokens, device=dev) for _ in range(S)]
     buf = bufs[0]
+    ann = None
+    if args.retriever == "ann":
+        assert w.shared_bank, "the graph-ANN backend indexes one shared bank"
+        beam = args.beam or next(b for b in (64, 128, 256) if b >= w.k)
+        tb = time.time()
+        index = AnnIndex(bank, degree=args.degree, n_seeds=args.seeds)
+        torch.cuda.synchronize()
+        ann = {"degree": args.degree, "beam": beam, "width": args.width,
+               "n_seeds": index.n_seeds, "max_iters": args.max_iters,
+               "build_s": round(time.time() - tb, 2)}
+        log(f"ANN index: degree {args.degree}, {index.n_seeds} seeds, built in "
+            f"{ann['build_s']} s")
+        for b in bufs:
+            b.ann_iters = torch.zeros(w.nq, dtype=torch.int32, device=dev)
+            b.ann_scored = torch.zeros(w.nq, dtype=torch.int32, device=dev)
+
+    def retrieve(q, b):
+        if ann is None:
+            b.retrieve(q, bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        else:
+            index.search(q, b.ids, nq=w.nq, k=w.k, beam=ann["beam"], width=ann["width"],
+                         max_iters=ann["max_iters"], out_scores=b.scores, out_iters=b.ann_iters,
+                         out_scored=b.ann_scored)
+
     lens, offs = store["fact_lens"], store["fact_offsets"]
     lens_stride = 0 if lens.shape[0] == 1 else w.n
     L, T, H, D = store["preK"].shape
@@ -152,7 +185,7 @@ def main():
 
     def step(i, b=None):
         b = buf if b is None else b
-        b.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        retrieve(queries[i], b)
         for j in range(nwaves):
             place(i, j, b)
             inject(j, b)
@@ -198,7 +231,10 @@ def main():
                            max_tokens=w.max_tokens, device=dev, workspace=buf.workspace)
             for _ in range(args.steps)]
     for si, i in enumerate(range(args.warmup, nsteps)):
-        sets[si].retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        if ann is not None:
+            sets[si].ann_iters = torch.zeros(w.nq, dtype=torch.int32, device=dev)
+            sets[si].ann_scored = torch.zeros(w.nq, dtype=torch.int32, device=dev)
+        retrieve(queries[i], sets[si])
         for j in range(nwaves):
             place(i, j, sets[si])
     torch.cuda.synchronize()
@@ -211,6 +247,45 @@ def main():
     torch.cuda.synchronize()
     inj_launch_ms = ei0.elapsed_time(ei1) / (args.steps * nwaves)
     log(f"inject alone: {inj_launch_ms * 1e3:.1f} us per launch")
+
+    # ---- ANN: the search alone, the exact retrieval alone, recall ------------
+    if ann is not None:
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record()
+        for si, i in enumerate(range(args.warmup, nsteps)):
+            retrieve(queries[i], sets[si])
+        eb.record()
+        torch.cuda.synchronize()
+        search_ms = ea.elapsed_time(eb) / args.steps
+        exact = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
+                               max_tokens=1, device=dev)
+        hits, ex_ms = 0, []
+        for si, i in enumerate(range(args.warmup, nsteps)):
+            xa, xb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            xa.record()
+            exact.retrieve(queries[i], bank)
+            xb.record()
+            torch.cuda.synchronize()
+            ex_ms.append(xa.elapsed_time(xb))
+            got, want = sets[si].ids.cpu().tolist(), exact.ids.cpu().tolist()
+            hits += sum(len(set(a) & set(b)) for a, b in zip(got, want))
+        row_bytes = w.d_e * bank.element_size()
+        scored = statistics.fmean(float(b.ann_scored.double().mean()) for b in sets)
+        iters = statistics.fmean(float(b.ann_iters.double().mean()) for b in sets)
+        # rows read by the search + neighbour lists + the seed scan, per launch
+        ann_bytes = w.nq * (scored * row_bytes + iters * ann["width"] * args.degree * 4) \
+            + ann["n_seeds"] * row_bytes
+        ann.update({
+            "recall_at_k": round(hits / (args.steps * w.nq * w.k), 4),
+            "iters_mean": round(iters, 1), "rows_read_per_query": round(scored, 1),
+            "search_us": round(search_ms * 1e3, 1),
+            "exact_retrieve_us": round(statistics.median(ex_ms) * 1e3, 1),
+            "search_bytes_per_launch": round(ann_bytes),
+            "search_GBps": round(ann_bytes / (search_ms * 1e-3) / 1e9, 1),
+        })
+        log(f"ANN: recall@{w.k} {ann['recall_at_k']}, {iters:.1f} iterations, {scored:.0f} rows "
+            f"per query; search {ann['search_us']} us vs exact {ann['exact_retrieve_us']} us "
+            f"per launch; {ann['search_GBps']} GB/s")
 
     # ---- optional: the consumer of the pages, every layer of every request ---
     consumer = None
@@ -247,7 +322,7 @@ def main():
     for i in (range(args.warmup, nsteps) if args.detail else ()):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * nwaves)]
         e[0].record()
-        buf.retrieve(queries[i], bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+        retrieve(queries[i], buf)
         e[1].record()
         for j in range(nwaves):
             place(i, j)
@@ -288,13 +363,13 @@ def main():
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
-            buf.retrieve(qbuf, bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+            retrieve(qbuf, buf)
             place(0, 0)
             inject(0)
         torch.cuda.current_stream().wait_stream(s)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            buf.retrieve(qbuf, bank, bank_stride=0 if w.shared_bank else w.n * w.d_e)
+            retrieve(qbuf, buf)
             place(0, 0)
             inject(0)
         torch.cuda.synchronize()
@@ -325,7 +400,7 @@ def main():
 
     # ---- CPU baseline: the oracle on the host for a bounded sample ------------
     cpu = None
-    if not args.no_cpu_baseline and args.workload == "llama8b" and not host_store:
+    if not args.no_cpu_baseline and args.workload == "llama8b" and not host_store and ann is None:
         cpu = cpu_baseline(w, bank, store, queries, bts, args, torch)
 
     out = {
@@ -353,6 +428,9 @@ def main():
             "rope": {"default": f"theta^(-2j/D), pairs (j, j+D/2)",
                      "llama3.1": "Llama 3.1 scaled table, pairs (j, j+D/2)",
                      "interleaved": "theta^(-2j/D), pairs (2j, 2j+1)"}[args.rope],
+            "retriever": ("exact" if ann is None else
+                          f"graph ANN (degree {ann['degree']}, beam {ann['beam']}, "
+                          f"width {ann['width']}, {ann['n_seeds']} seeds)"),
             "store": ("pinned host memory, read over PCIe "
                       f"({w.payloads} payloads, {2 * store['preK'].numel() * 2 / 1e9:.1f} GB)"
                       if host_store else "HBM"),
@@ -364,12 +442,13 @@ def main():
         "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),
-        "retrieve": None if ret_ms is None else {
+        "retrieve": None if ret_ms is None or ann is not None else {
             "us": round(ret_ms * 1e3, 2), "bank_bytes": scan_bytes,
             "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
             "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "consumer": consumer,
+        "ann": ann,
         "roofline": {
             "bound": "hbm",
             "kernel": "inject_kernel",

@@ -333,8 +333,14 @@ int is_ann_search_workspace_size(int32_t n_seeds, int32_t d, int32_t beam, int32
  *   width      1 <= width <= IS_ANN_MAX_WIDTH, width * degree <=
  *              IS_ANN_MAX_EXPAND
  *   max_iters  >= 0 (0: the best seeds)
+ * Scores: fp32 sums of the exact products; bf16 rows add two products per
+ * packed dot step (round to nearest even, within about one ulp per step),
+ * fp32 rows use fused multiply-adds.
  *   out_ids    int32 [nq][k]; out_scores fp32 [nq][k] or NULL; out_iters
- *              int32 [nq] or NULL; all device
+ *              int32 [nq] or NULL; out_scored int32 [nq] or NULL: bank rows
+ *              the search read for the query (each fact at most once while
+ *              it is remembered as scored; the seed retrieval not counted);
+ *              all device
  *   status     device flag word or NULL: a graph entry or seed id outside
  *              [0, n) sets IS_DEV_ID_RANGE and is skipped
  *   workspace  at least is_ann_search_workspace_size bytes, 256-byte aligned
@@ -343,7 +349,8 @@ int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n
                   int32_t dtype, const int32_t* graph, int32_t degree, const int32_t* seed_ids,
                   const void* seed_bank, int32_t n_seeds, int32_t beam, int32_t width, int32_t k,
                   int32_t max_iters, int32_t* out_ids, float* out_scores, int32_t* out_iters,
-                  uint32_t* status, void* workspace, size_t workspace_bytes, void* stream);
+                  int32_t* out_scored, uint32_t* status, void* workspace, size_t workspace_bytes,
+                  void* stream);
 
 #ifdef __cplusplus
 }

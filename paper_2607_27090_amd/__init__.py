@@ -96,7 +96,7 @@ def load_library() -> ctypes.CDLL:
     lib.is_ann_search_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.is_ann_search_workspace_size.restype = ctypes.c_int
     lib.is_ann_search.argtypes = [P, i32, P, i64, i32, i32, P, i32, P, P, i32, i32, i32, i32,
-                                  i32, P, P, P, P, P, sz, P]
+                                  i32, P, P, P, P, P, P, sz, P]
     lib.is_ann_search.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -259,7 +259,7 @@ def is_ann_search_workspace_size(n_seeds: int, d: int, beam: int, nq: int = 1,
 
 def is_ann_search(query_emb, bank, n, d, graph, degree, seed_ids, seed_bank, out_ids, *,
                   nq=1, n_seeds, beam=64, width=1, k, max_iters, out_scores=None, out_iters=None,
-                  status=None, workspace=None, stream=None) -> None:
+                  out_scored=None, status=None, workspace=None, stream=None) -> None:
     """Beam search over the proximity graph (see include/inferscale.h)."""
     dt = _emb_dtype(query_emb)
     if workspace is None:
@@ -269,4 +269,5 @@ def is_ann_search(query_emb, bank, n, d, graph, degree, seed_ids, seed_bank, out
     _check("is_ann_search", load_library().is_ann_search(
         _ptr(query_emb), nq, _ptr(bank), n, d, dt, _ptr(graph), degree, _ptr(seed_ids),
         _ptr(seed_bank), n_seeds, beam, width, k, max_iters, _ptr(out_ids), _ptr(out_scores),
-        _ptr(out_iters), _ptr(status), _ptr(workspace), ws_bytes, _stream(stream)))
+        _ptr(out_iters), _ptr(out_scored), _ptr(status), _ptr(workspace), ws_bytes,
+        _stream(stream)))

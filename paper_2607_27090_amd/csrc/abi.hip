@@ -535,7 +535,8 @@ int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n
                   int32_t dtype, const int32_t* graph, int32_t degree, const int32_t* seed_ids,
                   const void* seed_bank, int32_t n_seeds, int32_t beam, int32_t width, int32_t k,
                   int32_t max_iters, int32_t* out_ids, float* out_scores, int32_t* out_iters,
-                  uint32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+                  int32_t* out_scored, uint32_t* status, void* workspace, size_t workspace_bytes,
+                  void* stream) {
     if (!query_emb || !bank || !graph || !seed_ids || !seed_bank || !out_ids)
         return fail(IS_ERR_INVALID,
                     "query_emb, bank, graph, seed_ids, seed_bank and out_ids must be non-NULL");
@@ -545,7 +546,7 @@ int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n
         return fail(IS_ERR_INVALID, "query_emb, bank and seed_bank must be 16-byte aligned");
     if (!aligned(graph, 4) || !aligned(seed_ids, 4) || !aligned(out_ids, 4) ||
         (out_scores && !aligned(out_scores, 4)) || (out_iters && !aligned(out_iters, 4)) ||
-        (status && !aligned(status, 4)))
+        (out_scored && !aligned(out_scored, 4)) || (status && !aligned(status, 4)))
         return fail(IS_ERR_INVALID, "misaligned pointer argument");
     const AnnSearchLayout lay = ann_search_layout(n_seeds, d, beam, nq, dtype);
     if (!workspace || workspace_bytes < lay.total)
@@ -562,7 +563,8 @@ int is_ann_search(const void* query_emb, int32_t nq, const void* bank, int64_t n
     if (rc) return rc;
     hipError_t e = is::launch_ann_search(query_emb, nq, bank, n, d, dtype, graph, degree, seed_ids,
                                          n_seeds, init_ids, init_scores, lay.n_init, beam, width,
-                                         k, max_iters, out_ids, out_scores, out_iters, status, st);
+                                         k, max_iters, out_ids, out_scores, out_iters, out_scored,
+                                         status, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "graph search launch: %s", hipGetErrorString(e));
     return ok();
 }

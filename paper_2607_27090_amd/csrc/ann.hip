@@ -339,7 +339,8 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
     const int32_t* __restrict__ graph, int R, const int32_t* __restrict__ seed_ids,
     int n_seeds, const int32_t* __restrict__ init_local, const float* __restrict__ init_score,
     int n_init, int B, int P, int k, int max_iters, int32_t* __restrict__ out_ids,
-    float* __restrict__ out_scores, int32_t* __restrict__ out_iters, uint32_t* __restrict__ status) {
+    float* __restrict__ out_scores, int32_t* __restrict__ out_iters,
+    int32_t* __restrict__ out_scored, uint32_t* __restrict__ status) {
     constexpr int NR = E >= 32 ? 1 : 32 / E;
     __shared__ SearchShared sh;
     const int t = threadIdx.x;
@@ -390,7 +391,7 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
     }
     if (t == 0) sh.hcount = nvalid;
     __syncthreads();
-    int nb = nvalid, cur = 0, iters = 0;
+    int nb = nvalid, cur = 0, iters = 0, scored = 0;
 
     while (iters < max_iters) {
         // ---- A. the first P unexpanded entries ----
@@ -428,6 +429,7 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
         const int cpos = block_compact(fresh, sh, &C);
         if (fresh) sh.cand_id[cpos] = j;
         if (t == 0) sh.hcount += C;
+        scored += C;
         __syncthreads();
 
         // ---- C. scores: row group g takes rows g, g + 16, ... Every
@@ -506,6 +508,7 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
     }
     if (t == 0) {
         if (out_iters) out_iters[q] = iters;
+        if (out_scored) out_scored[q] = scored;
         if (status && sh.flags) atomicOr(status, sh.flags);
     }
 }
@@ -584,13 +587,13 @@ static hipError_t launch_search_tag(int E, const void* query, int nq, const void
                                     const int32_t* seed_ids, int n_seeds,
                                     const int32_t* init_local, const float* init_score, int n_init,
                                     int B, int P, int k, int max_iters, int32_t* out_ids,
-                                    float* out_scores, int32_t* out_iters, uint32_t* status,
-                                    hipStream_t st) {
+                                    float* out_scores, int32_t* out_iters, int32_t* out_scored,
+                                    uint32_t* status, hipStream_t st) {
 #define IS_ANN_LAUNCH(EE)                                                                         \
     hipLaunchKernelGGL((ann_search_kernel<Tag, EE>), dim3(nq), dim3(kSrchThreads), 0, st,         \
                        (const uint4*)query, (const uint4*)bank, n, row_chunks, graph, R, seed_ids, \
                        n_seeds, init_local, init_score, n_init, B, P, k, max_iters, out_ids,      \
-                       out_scores, out_iters, status)
+                       out_scores, out_iters, out_scored, status)
     switch (E) {
         case 1: IS_ANN_LAUNCH(1); break;
         case 2: IS_ANN_LAUNCH(2); break;
@@ -607,18 +610,19 @@ hipError_t launch_ann_search(const void* query, int nq, const void* bank, int64_
                              int dtype, const int32_t* graph, int R, const int32_t* seed_ids,
                              int n_seeds, const int32_t* init_local, const float* init_score,
                              int n_init, int B, int P, int k, int max_iters, int32_t* out_ids,
-                             float* out_scores, int32_t* out_iters, uint32_t* status,
-                             hipStream_t st) {
+                             float* out_scores, int32_t* out_iters, int32_t* out_scored,
+                             uint32_t* status, hipStream_t st) {
     const int row_chunks = d * (dtype == IS_DTYPE_F32 ? 4 : 2) / 16;
     int E = 1;
     while (E * kRowLanes < row_chunks) E <<= 1;
     if (dtype == IS_DTYPE_F32)
         return launch_search_tag<F32Tag>(E, query, nq, bank, n, row_chunks, graph, R, seed_ids,
                                          n_seeds, init_local, init_score, n_init, B, P, k,
-                                         max_iters, out_ids, out_scores, out_iters, status, st);
+                                         max_iters, out_ids, out_scores, out_iters, out_scored,
+                                         status, st);
     return launch_search_tag<BF16Tag>(E, query, nq, bank, n, row_chunks, graph, R, seed_ids,
                                       n_seeds, init_local, init_score, n_init, B, P, k, max_iters,
-                                      out_ids, out_scores, out_iters, status, st);
+                                      out_ids, out_scores, out_iters, out_scored, status, st);
 }
 
 }  // namespace is

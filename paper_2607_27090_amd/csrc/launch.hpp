@@ -80,7 +80,7 @@ hipError_t launch_ann_search(const void* query, int nq, const void* bank, int64_
                              int dtype, const int32_t* graph, int R, const int32_t* seed_ids,
                              int n_seeds, const int32_t* init_local, const float* init_score,
                              int n_init, int B, int P, int k, int max_iters, int32_t* out_ids,
-                             float* out_scores, int32_t* out_iters, uint32_t* status,
-                             hipStream_t st);
+                             float* out_scores, int32_t* out_iters, int32_t* out_scored,
+                             uint32_t* status, hipStream_t st);
 
 }  // namespace is

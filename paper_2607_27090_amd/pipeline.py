@@ -111,9 +111,11 @@ class AnnIndex:
         return self._ws[key]
 
     def search(self, query, out_ids, *, nq: int, k: int, beam: int = 64, width: int = 1,
-               max_iters: int = 256, out_scores=None, out_iters=None, status=None, stream=None):
+               max_iters: int = 256, out_scores=None, out_iters=None, out_scored=None, status=None,
+               stream=None):
         is_ann_search(query, self.bank, self.n, self.d, self.graph, self.degree, self.seed_ids,
                       self.seed_bank, out_ids, nq=nq, n_seeds=self.n_seeds, beam=beam,
                       width=width, k=k, max_iters=max_iters, out_scores=out_scores,
-                      out_iters=out_iters, status=status, workspace=self.workspace(nq, beam),
+                      out_iters=out_iters, out_scored=out_scored, status=status,
+                      workspace=self.workspace(nq, beam),
                       stream=stream)

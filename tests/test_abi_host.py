@@ -200,12 +200,12 @@ def test_ann_build_rejects(kw, code):
 
 def _ann_search(**kw):
     a = dict(q=A, nq=4, bank=A, n=1000, d=64, dt=1, G=A, R=16, sid=A, sb=A, ns=8, B=64, P=1,
-             k=10, T=100, ids=A, sc=None, it=None, st=None, ws=A, wsb=1 << 34)
+             k=10, T=100, ids=A, sc=None, it=None, ev=None, st=None, ws=A, wsb=1 << 34)
     a.update(kw)
     return isl.load_library().is_ann_search(
         a["q"], a["nq"], a["bank"], a["n"], a["d"], a["dt"], a["G"], a["R"], a["sid"], a["sb"],
-        a["ns"], a["B"], a["P"], a["k"], a["T"], a["ids"], a["sc"], a["it"], a["st"], a["ws"],
-        a["wsb"], None)
+        a["ns"], a["B"], a["P"], a["k"], a["T"], a["ids"], a["sc"], a["it"], a["ev"], a["st"],
+        a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -220,7 +220,8 @@ def _ann_search(**kw):
     (dict(P=3, R=100), isl.IS_ERR_INVALID), (dict(k=0), isl.IS_ERR_INVALID),
     (dict(k=65), isl.IS_ERR_INVALID), (dict(T=-1), isl.IS_ERR_INVALID),
     (dict(q=A + 4), isl.IS_ERR_INVALID), (dict(sb=A + 8), isl.IS_ERR_INVALID),
-    (dict(it=A + 2), isl.IS_ERR_INVALID), (dict(ws=None), isl.IS_ERR_WORKSPACE),
+    (dict(it=A + 2), isl.IS_ERR_INVALID), (dict(ev=A + 2), isl.IS_ERR_INVALID),
+    (dict(ws=None), isl.IS_ERR_WORKSPACE),
     (dict(wsb=512), isl.IS_ERR_WORKSPACE),
 ])
 def test_ann_search_rejects(kw, code):

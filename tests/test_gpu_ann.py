@@ -88,14 +88,19 @@ def run_search(bank, graph, seeds, query, *, beam, width, k, max_iters, status=N
     ids = torch.full((nq, k), -7, dtype=torch.int32, device="cuda")
     sc = torch.empty(nq, k, dtype=torch.float32, device="cuda")
     it = torch.empty(nq, dtype=torch.int32, device="cuda")
+    ev = torch.empty(nq, dtype=torch.int32, device="cuda")
     dt = 0 if bank.dtype == torch.float32 else 1
     ws = torch.empty(max(256, is_ann_search_workspace_size(len(seeds), d, beam, nq, dt)),
                      dtype=torch.uint8, device="cuda")
     is_ann_search(query, bank, n, d, g, R, s, sb, ids, nq=nq, n_seeds=len(seeds), beam=beam,
                   width=width, k=k, max_iters=max_iters, out_scores=sc, out_iters=it,
-                  status=status, workspace=ws)
+                  out_scored=ev, status=status, workspace=ws)
     torch.cuda.synchronize()
-    return ids.cpu().numpy(), sc.cpu().numpy(), it.cpu().numpy()
+    it_, ev_ = it.cpu().numpy(), ev.cpu().numpy()
+    # rows read: at most every neighbour of every expanded fact
+    assert (ev_ >= 0).all() and (ev_ <= it_ * width * R).all()
+    assert (ev_[it_ == 0] == 0).all()
+    return ids.cpu().numpy(), sc.cpu().numpy(), it_
 
 
 def check_search(bank, graph, seeds, query, **kw):
