@@ -34,18 +34,25 @@ constexpr int kAnnMaxWidth = IS_ANN_MAX_WIDTH;
 // ---- build: forward lists --------------------------------------------------
 
 // ids [nb][R + 1] ranked neighbours of rows row0 .. row0 + nb - 1 (each row's
-// own id among them unless R + 1 rows tie above it) -> F[row][0 .. R).
+// own id among them unless R + 1 rows tie above it) -> F[row][0 .. R): the
+// list in order without the row itself, first R entries. One wave per row.
 __global__ void ann_take_kernel(const int32_t* __restrict__ ids, int64_t row0, int nb, int R,
                                 int32_t* __restrict__ F) {
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int b = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
     if (b >= nb) return;
     const int64_t self = row0 + b;
     const int32_t* src = ids + (int64_t)b * (R + 1);
     int32_t* dst = F + self * R;
-    int o = 0;
-    for (int r = 0; r <= R && o < R; ++r) {
-        const int32_t j = src[r];
-        if (j != self) dst[o++] = j;
+    int dropped = 0;
+    for (int base = 0; base <= R; base += kWave) {
+        const int r = base + lane;
+        const int32_t j = r <= R ? src[r] : -1;
+        const bool drop = r <= R && j == self;
+        const uint64_t m = __ballot(drop);
+        const int pos = r - dropped - (int)lanes_below(m);
+        if (r <= R && !drop && pos < R) dst[pos] = j;
+        dropped += __popcll(m);
     }
 }
 
@@ -517,7 +524,7 @@ __global__ __launch_bounds__(kSrchThreads) void ann_search_kernel(
 
 hipError_t launch_ann_take(const int32_t* ids, int64_t row0, int nb, int R, int32_t* F,
                            hipStream_t st) {
-    hipLaunchKernelGGL(ann_take_kernel, dim3((nb + 255) / 256), dim3(256), 0, st, ids, row0, nb,
+    hipLaunchKernelGGL(ann_take_kernel, dim3((nb + 3) / 4), dim3(4 * kWave), 0, st, ids, row0, nb,
                        R, F);
     return hipGetLastError();
 }
