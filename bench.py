@@ -286,6 +286,9 @@ def main():
         log(f"ANN: recall@{w.k} {ann['recall_at_k']}, {iters:.1f} iterations, {scored:.0f} rows "
             f"per query; search {ann['search_us']} us vs exact {ann['exact_retrieve_us']} us "
             f"per launch; {ann['search_GBps']} GB/s")
+        if not args.no_cpu_baseline:
+            ann["cpu_baseline"] = ann_cpu_baseline(w, bank, index, queries[args.warmup], ann,
+                                                   args, torch)
 
     # ---- optional: the consumer of the pages, every layer of every request ---
     consumer = None
@@ -493,6 +496,32 @@ def measured_traffic():
             if hashlib.sha256(f.read()).hexdigest() != digest:
                 return None
     return tb if want else None
+
+
+def ann_cpu_baseline(w, bank, index, query, ann, args, torch):
+    """The oracle's beam search (oracle/ann.c, one thread) over the same graph
+    and seeds, one query at a time, for about half of --cpu-seconds."""
+    import numpy as np
+    import oracle
+
+    def host(t):
+        if t.dtype == torch.float32:
+            return t.contiguous().cpu().numpy(), oracle.F32
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16), oracle.BF16
+
+    bh, odt = host(bank)
+    qh, _ = host(query)
+    G = index.graph.cpu().numpy()
+    seeds = index.seed_ids.cpu().numpy()
+    t0, done = time.perf_counter(), 0
+    while done < w.nq and time.perf_counter() - t0 < args.cpu_seconds / 2:
+        oracle.ann_search(qh[done:done + 1], bh, w.n, w.d_e, G, seeds, ann["beam"], w.k,
+                          ann["max_iters"], width=ann["width"], dtype=odt)
+        done += 1
+    el = time.perf_counter() - t0
+    log(f"cpu oracle (graph search): {done} queries, {el:.1f}s")
+    return {"value": round(el / done * 1e6, 1), "unit": "us/query", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of the {w.nq} queries of one step, the same graph and seeds"}
 
 
 def cpu_baseline(w, bank, store, queries, bts, args, torch):
