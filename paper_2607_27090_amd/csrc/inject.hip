@@ -6,33 +6,50 @@
 // times the model's own rotary table, §3.3 and §6.1).
 //
 // Work decomposition (HBM-bound streaming copy with a little math):
-//   * a thread item is (placed token, 16-element lane unit of a head): it owns
-//     elements [8u, 8u+8) of the first half of head h and the matching
+//   * a lane item is (placed token, 16-element lane unit of a head): the lane
+//     owns elements [8u, 8u+8) of the first half of head h and the matching
 //     elements [D/2 + 8u, D/2 + 8u + 8) of the second half, so every rotation
-//     pair lives in one thread in both pair layouts -- (j, j + D/2), the
+//     pair lives in one lane in both pair layouts -- (j, j + D/2), the
 //     half-split one, and (2j, 2j + 1), the interleaved one -- and all
-//     loads/stores are 16 bytes;
-//     one wave covers one full (token, layer) row of H*D elements when
-//     H*D == 1024, i.e. 2 KiB of K and 2 KiB of V, read and written as whole
-//     128-byte lines;
-//   * a work unit is (256 consecutive thread items, one layer), ordered token
-//     block first; every block of a fixed, persistent grid (~4 per CU, set by
-//     max_tokens only) takes one contiguous, equal share of its request's
-//     units, reading m from device memory, so a request can be enqueued (or
-//     captured in a graph) with no host round trip and no tail imbalance;
-//   * the 8 angles of a thread depend only on its token's position, so their
-//     fp64 reduction and fp32 sincos are paid once per token block of the
-//     share and reused for every layer in it;
-//   * layers are processed kUnroll at a time with unconditional loads, so
-//     each thread keeps 4 * kUnroll independent 16-byte loads in flight and
-//     the staging stays in registers.
+//     loads/stores are 16 bytes; one wave covers 64 consecutive lane items,
+//     i.e. one full (token, layer) row of H*D elements when H*D == 1024
+//     (2 KiB of K and 2 KiB of V, read and written as whole 128-byte lines);
+//   * a work item is (64 consecutive lane items, kInjLayers consecutive
+//     layers), numbered layer-group major; a request's work items are split
+//     into equal contiguous shares, one per workgroup;
+//   * a workgroup is 16 waves and occupies a whole CU (the launch reserves
+//     more than half of the CU's LDS), and its waves take the share's work
+//     items one at a time from a counter in LDS. The hardware issues the
+//     memory instructions of older waves first, so waves of one CU progress
+//     at very different rates; taking items from a shared counter lets the
+//     favoured waves do more of them, where equal static shares per wave or
+//     per co-resident workgroup left the least favoured finishing last;
+//   * each item's 8 angles per lane (fp64 reduction + fp32 sincos) are
+//     computed while its loads are in flight;
+//   * loads and stores are non-temporal: every stored byte is read once and
+//     every page byte is written once.
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace is {
 
-constexpr int kInjThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kInjThreads = 1024;  // 16 waves: one workgroup fills a CU
+constexpr int kInjLayers = 2;      // layers of one work item
+// dynamic LDS requested beyond the kernel's own, so that no two workgroups
+// share a CU (160 KiB of LDS per CU)
+constexpr size_t kInjLdsReserve = 84 * 1024;
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte non-temporal load / store (streamed: read once, written once)
+__device__ __forceinline__ uint4 load_nt(const uint4* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store_nt(uint4* p, uint4 v) {
+    const u32x4_t x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+}
 
 __device__ __forceinline__ void rotate8(const uint4 lo, const uint4 hi, const float (&c)[8],
                                         const float (&s)[8], uint4& out_lo, uint4& out_hi) {
@@ -74,7 +91,7 @@ __device__ __forceinline__ void rotate8_interleaved(const uint4 lo, const uint4 
 }
 
 template <bool INTERLEAVED>
-__global__ __launch_bounds__(kInjThreads, 4) void inject_kernel(
+__global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     const int32_t* __restrict__ ids, const uint4* __restrict__ preK, const uint4* __restrict__ V,
     const int64_t* __restrict__ slots, const int32_t* __restrict__ positions, float rope_theta,
     uint4* __restrict__ paged_k, uint4* __restrict__ paged_v,
@@ -88,207 +105,169 @@ __global__ __launch_bounds__(kInjThreads, 4) void inject_kernel(
     __shared__ int64_t s_wave_tot[kInjThreads / kWave];
     __shared__ uint32_t s_flags;
     __shared__ int32_t s_bad;
+    __shared__ int32_t s_next;                // next work item of the share
 
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r = blockIdx.y;
-    const int32_t* rid = ids + (int64_t)r * k;
-    // issue the independent loads first: m, this thread's (up to 4) fact ids
-    // of the placement order, and below the first unit's slot and position
+    // m and this thread's fact id (fact t of the placement order, k <= the
+    // block size) are independent loads; the fact's length and store row
+    // depend only on the id and are loaded together
     const int32_t m_in = m_dev[r];
-    int32_t cid[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = 4 * t + e;
-        cid[e] = i < k ? (reverse_rank ? rid[k - 1 - i] : rid[i]) : 0;
-    }
+    const int32_t* rid = ids + (int64_t)r * k;
+    const int32_t cid = t < k ? (reverse_rank ? rid[k - 1 - t] : rid[t]) : 0;
     const int32_t m = min(m_in, max_tokens);
     if (m <= 0) return;
-    const int lpu = D >> 4;              // lane units per head
-    const int U = H * lpu;               // lane units per (token, layer) row
-
-    // Work units are (token block of kInjThreads items, layer), token-block
-    // major. Each block takes one contiguous, equal share of the units, so
-    // consecutive units usually share a token block and its angles.
-    const int64_t items = (int64_t)m * U;
-    const int64_t ntb = (items + kInjThreads - 1) / kInjThreads;
-    const int64_t total = ntb * L;
-    const int64_t u0 = total * blockIdx.x / gridDim.x;
-    const int64_t u1 = total * (blockIdx.x + 1) / gridDim.x;
-    const int64_t* slots_r = slots + (int64_t)r * max_tokens;
-    const int32_t* pos_r = positions + (int64_t)r * max_tokens;
-    const int64_t pf_tb = u0 < u1 ? u0 / L : -1;
-    int64_t pf_slot = -1;
-    int32_t pf_pos = 0;
-    if (pf_tb >= 0 && pf_tb * kInjThreads + t < items) {
-        const int64_t tok = (pf_tb * kInjThreads + t) / U;
-        pf_slot = slots_r[tok];
-        pf_pos = pos_r[tok];
-    }
 
     // ---- per-request setup: placement offsets, store rows, frequencies ----
-    if (t == 0) { s_flags = 0; s_bad = 0; }
-    __syncthreads();
     const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
     const int64_t* offs = fact_offsets + (int64_t)r * lens_stride;
-    // each thread owns up to 4 consecutive facts of the placement order
-    int32_t my_len[4];
-    int64_t run = 0;
     uint32_t flags = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = 4 * t + e;
-        int32_t len = 0;
-        if (i < k) {
-            const int32_t c = cid[e];
-            int64_t off = -1;
-            if (c < 0 || (int64_t)c >= n) {
-                flags |= IS_DEV_ID_RANGE;
+    int64_t len = 0;
+    if (t < k) {
+        int64_t off = -1;
+        if (cid < 0 || (int64_t)cid >= n) {
+            flags |= IS_DEV_ID_RANGE;
+        } else {
+            const int32_t l = lens[cid];
+            const int64_t o = offs[cid];
+            if (l < 0) {
+                flags |= IS_DEV_BAD_LEN;
             } else {
-                len = lens[c];
-                if (len < 0) {
-                    flags |= IS_DEV_BAD_LEN;
-                    len = 0;
-                } else {
-                    off = offs[c];
-                    if (off < 0 || off + len > T_store) {
-                        flags |= IS_DEV_SRC_RANGE;
-                        off = -1;
-                    }
-                }
+                len = l;
+                if (o < 0 || o + l > T_store) flags |= IS_DEV_SRC_RANGE;
+                else off = o;
             }
-            s_off[i] = off;
         }
-        my_len[e] = len;
-        run += len;
+        s_off[t] = off;
     }
-    if (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN)) s_bad = 1;
-    // exclusive scan of per-thread totals
-    const int64_t incl = wave_incl_scan(run, lane);
+    if (t == 0) { s_flags = 0; s_bad = 0; s_next = 0; }
+    const int64_t incl = wave_incl_scan(len, lane);
     if (lane == 63) s_wave_tot[wave] = incl;
     if (t < (D >> 1))
         s_invf[t] = inv_freq ? inv_freq[t]
                              : exp2(-(2.0 * (double)t / (double)D) * log2((double)rope_theta));
     __syncthreads();
-    int64_t excl = incl - run;
+    if (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN)) s_bad = 1;
+    int64_t excl = incl - len;
     for (int w = 0; w < wave; ++w) excl += s_wave_tot[w];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = 4 * t + e;
-        if (i < k) s_b[i] = excl;
-        excl += my_len[e];
-    }
+    if (t < k) s_b[t] = excl;
     if (t == 0) {
         int64_t tot = 0;
         for (int w = 0; w < kInjThreads / kWave; ++w) tot += s_wave_tot[w];
         s_b[k] = tot;
     }
+    if (t < k && (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN))) atomicOr(&s_flags, flags);
     __syncthreads();
     if (s_bad) {
         // a request with an invalid id or length is skipped as a whole
-        if (blockIdx.x == 0 && t == 0 && status) atomicOr(status, flags);
+        if (blockIdx.x == 0 && t == 0 && status) atomicOr(status, s_flags);
         return;
     }
     if (blockIdx.x != 0) flags = 0;  // fact-level flags are reported once per request
+
+    const int lpu = D >> 4;                         // lane units per head
+    const int U = H * lpu;                          // lane units per (token, layer) row
+    const int64_t items = (int64_t)m * U;
     // never place more tokens than the facts hold, whatever m says
-    const int64_t items_ok = min(items, s_b[k] * U);
+    const int64_t items_ok = min_i64(items, s_b[k] * U);
+    const int64_t ngroups = (items + kWave - 1) / kWave;      // 64-item groups
+    const int64_t nlg = (L + kInjLayers - 1) / kInjLayers;     // layer groups
+    const int64_t total = ngroups * nlg;
+    const int64_t i0 = total * blockIdx.x / gridDim.x;
+    const int64_t span = total * (blockIdx.x + 1) / gridDim.x - i0;
+    const int64_t* slots_r = slots + (int64_t)r * max_tokens;
+    const int32_t* pos_r = positions + (int64_t)r * max_tokens;
 
     const int64_t row_units = (int64_t)H * D / 8;  // 16-byte units per (token, layer) row
     const int half_units = D >> 4;                 // 16-byte units in half a head
-
     const int64_t sstride = T_store * row_units;    // one layer of the store
     const int64_t dstride = num_slots * row_units;  // one layer of the pages
-    // the slot and position of the next segment's token are loaded one
-    // segment ahead, so a segment switch does not wait on them
-    int64_t nx_slot = pf_slot;
-    int32_t nx_pos = pf_pos;
-    for (int64_t u = u0; u < u1;) {
-        const int64_t tb = u / L;
-        const int l0 = (int)(u - tb * L);
-        const int l1 = (int)min_i64(L, l0 + (u1 - u));
-        u += l1 - l0;
-        const int64_t slot_in = nx_slot;
-        const int32_t pos_in = nx_pos;
-        if (u < u1) {
-            const int64_t nitem = (u / L) * kInjThreads + t;
-            if (nitem < items_ok) {
-                const int64_t ntok = nitem / U;
-                nx_slot = slots_r[ntok];
-                nx_pos = pos_r[ntok];
+
+    int32_t j = 0;
+    if (lane == 0) j = atomicAdd(&s_next, 1);
+    j = __shfl(j, 0, kWave);
+    while ((int64_t)j < span) {
+        const int64_t wi = i0 + j;
+        // the wave's next item is taken now; the LDS round trip hides under
+        // this item's loads
+        int32_t jn = 0;
+        if (lane == 0) jn = atomicAdd(&s_next, 1);
+        const int64_t lg = wi / ngroups;
+        const int64_t item = (wi - lg * ngroups) * kWave + lane;
+        const int l0 = (int)lg * kInjLayers;
+        const int nl = min(kInjLayers, L - l0);
+        if (item < items_ok) {
+            const int32_t token = (int32_t)(item / U);
+            const int lu = (int)(item - (int64_t)token * U);
+            const int h = lu / lpu;
+            const int sub = lu - h * lpu;
+            // fact holding this placed token: last i with s_b[i] <= token
+            int lo = 0, hi = k - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_b[mid] <= token) lo = mid; else hi = mid - 1;
             }
-        }
-        const int64_t item = tb * kInjThreads + t;
-        if (item >= items_ok) continue;
-        const int32_t token = (int32_t)(item / U);
-        const int lu = (int)(item - (int64_t)token * U);
-        const int h = lu / lpu;
-        const int sub = lu - h * lpu;
-
-        // fact holding this placed token: last i with s_b[i] <= token
-        int lo = 0, hi = k - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (s_b[mid] <= token) lo = mid; else hi = mid - 1;
-        }
-        const int64_t off = s_off[lo];
-        if (off < 0) continue;
-        const int64_t src = off + (token - s_b[lo]);
-        const int64_t slot = slot_in;
-        if (slot < 0 || slot >= num_slots) { flags |= IS_DEV_SLOT_RANGE; continue; }
-
-        const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
-        const uint4* ksrc = preK + src * row_units + col;
-        const uint4* vsrc = V + src * row_units + col;
-        uint4* kdst = paged_k + slot * row_units + col;
-        uint4* vdst = paged_v + slot * row_units + col;
-
-        float cs[8], sn[8];
-        for (int l = l0; l < l1; l += kUnroll) {
-            // loads are unconditional (a short tail re-reads its last layer)
-            // so the staging arrays stay in registers
-            uint4 klo[kUnroll], khi[kUnroll], vlo[kUnroll], vhi[kUnroll];
+            const int64_t off = s_off[lo];
+            const int64_t slot = slots_r[token];
+            const int32_t pos = pos_r[token];
+            if (off >= 0) {
+                const int64_t src = off + (token - s_b[lo]);
+                const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
+                const uint4* ksrc = preK + src * row_units + col;
+                const uint4* vsrc = V + src * row_units + col;
+                // loads are unconditional (a short last layer group re-reads
+                // its last layer) so the staging stays in registers
+                uint4 klo[kInjLayers], khi[kInjLayers], vlo[kInjLayers], vhi[kInjLayers];
 #pragma unroll
-            for (int j = 0; j < kUnroll; ++j) {
-                const int64_t lj = min(l + j, l1 - 1);
-                klo[j] = ksrc[lj * sstride];
-                khi[j] = ksrc[lj * sstride + half_units];
-                vlo[j] = vsrc[lj * sstride];
-                vhi[j] = vsrc[lj * sstride + half_units];
-            }
-            if (l == l0) {
-                // the segment's angles, computed while its first loads are in
-                // flight: p * w_j formed in fp64, reduced to [-pi, pi] with a
+                for (int q = 0; q < kInjLayers; ++q) {
+                    const int64_t so = (int64_t)(l0 + min(q, nl - 1)) * sstride;
+                    klo[q] = load_nt(ksrc + so);
+                    khi[q] = load_nt(ksrc + so + half_units);
+                    vlo[q] = load_nt(vsrc + so);
+                    vhi[q] = load_nt(vsrc + so + half_units);
+                }
+                // the item's angles, computed while its loads are in flight:
+                // p * w_j formed in fp64, reduced to [-pi, pi] with a
                 // two-constant 2*pi, then fp32 sine and cosine
-                const double p = (double)pos_in;
+                float cs[8], sn[8];
+                const double p = (double)pos;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     // pair of angle e: half-split, j = 8 sub + e; interleaved,
                     // the 4 pairs of each 16-byte half, j = 4 sub + e and
                     // D/4 + 4 sub + e - 4
-                    const int j = INTERLEAVED ? (e < 4 ? 4 * sub + e : (D >> 2) + 4 * sub + e - 4)
-                                              : sub * 8 + e;
-                    const double a = p * s_invf[j];
+                    const int pj = INTERLEAVED ? (e < 4 ? 4 * sub + e : (D >> 2) + 4 * sub + e - 4)
+                                               : sub * 8 + e;
+                    const double a = p * s_invf[pj];
                     const double nrev = rint(a * 0.15915494309189535);
                     double red = fma(-nrev, 6.283185307179586, a);
                     red = fma(-nrev, 2.4492935982947064e-16, red);
                     sincosf((float)red, &sn[e], &cs[e]);
                 }
-            }
+                if (slot < 0 || slot >= num_slots) {
+                    flags |= IS_DEV_SLOT_RANGE;
+                } else {
+                    uint4* kdst = paged_k + slot * row_units + col;
+                    uint4* vdst = paged_v + slot * row_units + col;
 #pragma unroll
-            for (int j = 0; j < kUnroll; ++j) {
-                uint4 ylo, yhi;
-                if (INTERLEAVED)
-                    rotate8_interleaved(klo[j], khi[j], cs, sn, ylo, yhi);
-                else
-                    rotate8(klo[j], khi[j], cs, sn, ylo, yhi);
-                if (l + j < l1) {
-                    const int64_t dj = (int64_t)(l + j) * dstride;
-                    kdst[dj] = ylo;
-                    kdst[dj + half_units] = yhi;
-                    vdst[dj] = vlo[j];
-                    vdst[dj + half_units] = vhi[j];
+                    for (int q = 0; q < kInjLayers; ++q) {
+                        if (q < nl) {
+                            uint4 ylo, yhi;
+                            if (INTERLEAVED)
+                                rotate8_interleaved(klo[q], khi[q], cs, sn, ylo, yhi);
+                            else
+                                rotate8(klo[q], khi[q], cs, sn, ylo, yhi);
+                            const int64_t dq = (int64_t)(l0 + q) * dstride;
+                            store_nt(kdst + dq, ylo);
+                            store_nt(kdst + dq + half_units, yhi);
+                            store_nt(vdst + dq, vlo[q]);
+                            store_nt(vdst + dq + half_units, vhi[q]);
+                        }
+                    }
                 }
             }
         }
+        j = __shfl(jn, 0, kWave);
     }
     if (flags) atomicOr(&s_flags, flags);
     __syncthreads();
@@ -302,25 +281,39 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
                          int64_t T_store, int64_t num_slots, const double* inv_freq,
                          int32_t interleaved, uint32_t* status, hipStream_t st) {
+    if (k > kInjThreads) return hipErrorInvalidValue;
     const int64_t U = (int64_t)H * (D >> 4);
-    const int64_t ntb_max = ((int64_t)max_tokens * U + kInjThreads - 1) / kInjThreads;
-    if (ntb_max == 0) return hipSuccess;
-    // a fixed, persistent grid of ~4 blocks per CU shared by the requests;
-    // each block takes an equal share of its request's (token block, layer)
-    // units, so the shape depends on max_tokens only, never on m
+    const int64_t groups_max = ((int64_t)max_tokens * U + kWave - 1) / kWave;
+    const int64_t items_max = groups_max * ((L + kInjLayers - 1) / kInjLayers);
+    if (items_max == 0) return hipSuccess;
+    // one workgroup per CU, shared by the requests; the shape depends on
+    // max_tokens only, never on m
     const int cus = compute_units();
-    int64_t per_req = (4LL * cus + nq - 1) / nq;
-    if (per_req > ntb_max * L) per_req = ntb_max * L;
+    int64_t per_req = cus / nq;
+    if (per_req > items_max) per_req = items_max;
     if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
+    static bool lds_attr_set[64] = {false};
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
+        hipError_t e = hipFuncSetAttribute((const void*)inject_kernel<false>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)kInjLdsReserve);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void*)inject_kernel<true>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)kInjLdsReserve);
+        if (e != hipSuccess) return e;
+        lds_attr_set[dev] = true;
+    }
     if (interleaved)
-        hipLaunchKernelGGL(inject_kernel<true>, grid, dim3(kInjThreads), 0, st, ids,
+        hipLaunchKernelGGL(inject_kernel<true>, grid, dim3(kInjThreads), kInjLdsReserve, st, ids,
                            (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
                            (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
                            lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
                            inv_freq, status);
     else
-        hipLaunchKernelGGL(inject_kernel<false>, grid, dim3(kInjThreads), 0, st, ids,
+        hipLaunchKernelGGL(inject_kernel<false>, grid, dim3(kInjThreads), kInjLdsReserve, st, ids,
                            (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
                            (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
                            lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
