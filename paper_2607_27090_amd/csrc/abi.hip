@@ -125,7 +125,7 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
             : is::launch_scan(query_emb, bank, n, d, nq, bank_stride, dtype, scores, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
     if (lay.nchunks == 1) {
-        e = is::launch_select_scores(scores, n, k, nq, 1, nullptr, out_ids, out_scores, st);
+        e = is::launch_select_small(scores, n, k, nq, out_ids, out_scores, st);
         if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
         return ok();
     }

@@ -33,6 +33,9 @@ int64_t select_chunk_len();
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
                                 uint64_t* cand, int32_t* out_ids, float* out_scores,
                                 hipStream_t st);
+// Final ranking of one chunk of fp32 scores per query (n <= select_chunk_len()).
+hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, int32_t* out_ids,
+                               float* out_scores, hipStream_t st);
 hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, int nchunks,
                               uint64_t* cand, int32_t* out_ids, float* out_scores, hipStream_t st);
 // Final ranking from the sample winners first[q][k] and the filter survivors.

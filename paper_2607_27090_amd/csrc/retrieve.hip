@@ -492,6 +492,29 @@ __device__ __forceinline__ uint64_t wave_or64(uint64_t v) {
     return v;
 }
 
+// Exact rank of each of sh.cand[0 .. cand_total) (the number of larger
+// candidates; keys are distinct), writing the `want` best to sh.sel in rank
+// order: S consecutive lanes share a candidate and split its comparisons.
+// Ends with a barrier.
+__device__ __forceinline__ void rank_candidates(uint32_t cand_total, int want, SelShared& sh) {
+    const int t = threadIdx.x;
+    uint32_t S = 1;
+    while (S < 16 && 2 * S * cand_total <= (uint32_t)kSelThreads) S <<= 1;
+    const uint32_t part = (uint32_t)t & (S - 1);
+    for (uint32_t c = (uint32_t)t / S; c < cand_total; c += kSelThreads / S) {
+        const uint64_t me = sh.cand[c];
+        uint32_t rank = 0;
+        uint32_t j = part;
+        for (; j + 3 * S < cand_total; j += 4 * S)
+            rank += (sh.cand[j] > me) + (sh.cand[j + S] > me) + (sh.cand[j + 2 * S] > me) +
+                    (sh.cand[j + 3 * S] > me);
+        for (; j < cand_total; j += S) rank += sh.cand[j] > me;
+        for (uint32_t off = 1; off < S; off <<= 1) rank += __shfl_xor(rank, (int)off, kWave);
+        if (part == 0 && rank < (uint32_t)want) sh.sel[rank] = me;
+    }
+    __syncthreads();
+}
+
 // One block selects the `want` = min(k, valid keys) largest keys held in its
 // registers (kSelKpt per thread; keys are distinct: the low word is ~id, and
 // 0 marks an empty entry). On return sh.sel[0 .. want) holds them, best
@@ -563,23 +586,7 @@ __device__ int select_block(const uint64_t (&key)[kSelKpt], int k, SelShared& sh
             at += __popcll(mask[i]);
         }
         __syncthreads();
-        // exact rank of every candidate (the number of larger candidates):
-        // S consecutive lanes share a candidate and split its comparisons
-        uint32_t S = 1;
-        while (S < 16 && 2 * S * cand_total <= (uint32_t)kSelThreads) S <<= 1;
-        const uint32_t part = (uint32_t)t & (S - 1);
-        for (uint32_t c = (uint32_t)t / S; c < cand_total; c += kSelThreads / S) {
-            const uint64_t me = sh.cand[c];
-            uint32_t rank = 0;
-            uint32_t j = part;
-            for (; j + 3 * S < cand_total; j += 4 * S)
-                rank += (sh.cand[j] > me) + (sh.cand[j + S] > me) + (sh.cand[j + 2 * S] > me) +
-                        (sh.cand[j + 3 * S] > me);
-            for (; j < cand_total; j += S) rank += sh.cand[j] > me;
-            for (uint32_t off = 1; off < S; off <<= 1) rank += __shfl_xor(rank, (int)off, kWave);
-            if (part == 0 && rank < (uint32_t)want) sh.sel[rank] = me;
-        }
-        __syncthreads();
+        rank_candidates(cand_total, want, sh);
     } else {
         // many candidates: radix select the `want` largest among them
         uint64_t ref = 0, diff = 0;
@@ -709,6 +716,197 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     }
 }
 
+// Final top-k of at most kSelThreads * KPT fp32 scores per query, one block
+// per query (the single-chunk case: one query against a bank of up to 16,384
+// facts). Work is kept small because one CU does all of it:
+//  * thresholds are taken on the 32-bit order-preserving images of the
+//    scores (the id only breaks ties, so it is attached to candidates only);
+//  * the lower bound tau is the lower edge of a narrow bin holding the
+//    want-th largest thread maximum: radix passes of 8 bits over the thread
+//    maxima, from the highest bit where they differ, until at most 32 of them
+//    share the bin; at least `want` scores are >= tau and typically few more;
+//  * the candidates (valid, score bits >= tau) get their 64-bit rank keys,
+//    are compacted with wave ballots and ranked pairwise. Should there be
+//    more than kSelRankMax of them (many tied scores), the general select
+//    over 64-bit keys takes over.
+// Largest / smallest value over the 64 lanes of a wave (uniform result): DPP
+// quad, half-row and row exchanges give every lane its 16-lane row's value,
+// the four rows are combined in scalar registers.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return min(min(r0, r1), min(r2, r3));
+}
+
+// Final top-k of at most kSelThreads * KPT fp32 scores per query, one block
+// per query (the single-chunk case: one query against a bank of up to 16,384
+// facts). One CU does all of it, so the work per key is kept small:
+//  * thresholds are taken on the 32-bit order-preserving images of the
+//    scores (the id only breaks ties, so it is attached to candidates only);
+//  * the lower bound tau is the lower edge of a narrow bin holding the
+//    want-th largest thread maximum: radix passes of 8 bits over the thread
+//    maxima, from the highest bit where they differ, until at most 32 of them
+//    share the bin; at least `want` scores are >= tau and typically few more;
+//  * the candidates (valid, score bits >= tau) get their 64-bit rank keys,
+//    are gathered in LDS (each wave reserves its run with one atomic) and
+//    ranked pairwise. Should there be more than kSelRankMax of them (many
+//    tied scores), the general select over 64-bit keys takes over.
+template <int KPT>
+__global__ __launch_bounds__(kSelThreads) void select_small_kernel(
+    const float* __restrict__ scores, int64_t M, int k, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_scores) {
+    __shared__ SelShared sh;
+    __shared__ uint32_t s_hist2[256];   // radix passes alternate between sh.hist and this
+    __shared__ uint32_t s_ncand;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int q = blockIdx.y;
+    const float* sq = scores + (int64_t)q * M;
+    uint32_t u[KPT];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+        const int64_t idx = t + (int64_t)i * kSelThreads;  // coalesced
+        u[i] = idx < M ? score_order_bits(sq[idx]) : 0u;
+    }
+    const int want = (int)min_i64(k, M);
+    // the thread's keys are valid for i < nv (NaN scores are valid, lowest)
+    const int nv = M > t ? (int)min_i64(KPT, (M - t + kSelThreads - 1) / kSelThreads) : 0;
+    if (t == 0) s_ncand = 0;
+
+    // ---- 1. lower bound tau on the score bits ----
+    uint32_t tau = 0;  // every valid key is a candidate
+    if ((int64_t)want < M) {
+        uint32_t tm = 0;
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) tm = (i < nv && u[i] > tm) ? u[i] : tm;
+        // holders: the min(M, kSelThreads) >= want threads with a valid key
+        const uint32_t wmax = wave_max_u32(tm);
+        const uint32_t wmin = wave_min_u32(nv > 0 ? tm : 0xFFFFFFFFu);
+        if (lane == 0) {
+            sh.group[wave] = wmax;
+            sh.group[kSelWaves + wave] = wmin;
+        }
+        if (t < 256) {
+            sh.hist[t] = 0;
+            s_hist2[t] = 0;
+        }
+        __syncthreads();
+        uint32_t ref = 0, lowest = 0xFFFFFFFFu;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) {
+            ref = max(ref, (uint32_t)sh.group[w]);
+            lowest = min(lowest, (uint32_t)sh.group[kSelWaves + w]);
+        }
+        const uint32_t diff = ref ^ lowest;  // every holder's maximum lies in [lowest, ref]
+        if (diff == 0) {
+            tau = ref;
+        } else {
+            int hi = 31 - __builtin_clz(diff);
+            uint32_t pmask = hi == 31 ? 0u : ~((1u << (hi + 1)) - 1u);
+            uint32_t prefix = ref & pmask;
+            uint32_t need = (uint32_t)want;
+            for (int pass = 0;; ++pass) {
+                uint32_t* hist = (pass & 1) ? s_hist2 : sh.hist;
+                const int lo = max(0, hi - 7);
+                const uint32_t dmask = (1u << (hi - lo + 1)) - 1u;
+                if (nv > 0 && (tm & pmask) == prefix) atomicAdd(&hist[(tm >> lo) & dmask], 1u);
+                __syncthreads();
+                if (wave == 0) {
+                    // suffix sums over the bins (lane L owns bins 4L..4L+3); the
+                    // bin where the count of maxima from the top reaches `need`
+                    const uint32_t b0 = hist[4 * lane], b1 = hist[4 * lane + 1];
+                    const uint32_t b2 = hist[4 * lane + 2], b3 = hist[4 * lane + 3];
+                    const uint32_t mine = b0 + b1 + b2 + b3;
+                    uint32_t incl = mine;  // sum over lanes >= lane
+#pragma unroll
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const uint32_t o = __shfl_down(incl, off, kWave);
+                        if (lane + off < 64) incl += o;
+                    }
+                    const uint32_t a3 = incl - mine, a2 = a3 + b3, a1 = a2 + b2, a0 = a1 + b1;
+                    if (a3 < need && need <= a3 + b3) { sh.digit = 4 * lane + 3; sh.above = a3; sh.count = b3; }
+                    if (a2 < need && need <= a2 + b2) { sh.digit = 4 * lane + 2; sh.above = a2; sh.count = b2; }
+                    if (a1 < need && need <= a1 + b1) { sh.digit = 4 * lane + 1; sh.above = a1; sh.count = b1; }
+                    if (a0 < need && need <= a0 + b0) { sh.digit = 4 * lane; sh.above = a0; sh.count = b0; }
+                }
+                __syncthreads();
+                const uint32_t inbin = sh.count;
+                prefix |= sh.digit << lo;
+                pmask |= dmask << lo;
+                need -= sh.above;
+                // this pass's bins are cleared for the pass after next; the next
+                // pass's barrier orders the clearing before that pass's counts
+                // and wave 0's rewrite of digit / above / count after the reads
+                if (t < 256) hist[t] = 0;
+                if (inbin <= 32u || lo == 0) break;
+                hi = lo - 1;
+            }
+            tau = prefix;  // the lower edge of the bin: >= want maxima are >= tau
+        }
+    } else {
+        __syncthreads();  // s_ncand is cleared before any wave counts into it
+    }
+
+    // ---- 2. candidates: valid keys with score bits >= tau ----
+    uint64_t mask[KPT];
+    uint32_t wc = 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+        mask[i] = __ballot(i < nv && u[i] >= tau);
+        wc += __popcll(mask[i]);
+    }
+    uint32_t at = 0;
+    if (lane == 0 && wc) at = atomicAdd(&s_ncand, wc);
+    at = __shfl(at, 0, kWave);
+    if (wc) {
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+            if (mask[i]) {  // wave-uniform: most of the masks are empty
+                if (u[i] >= tau && i < nv) {
+                    const uint32_t idx = (uint32_t)(t + i * kSelThreads);
+                    const uint32_t slot = at + lanes_below(mask[i]);
+                    if (slot < (uint32_t)kSelRankMax)
+                        sh.cand[slot] = ((uint64_t)u[i] << 32) | (uint64_t)(~idx);
+                }
+                at += __popcll(mask[i]);
+            }
+        }
+    }
+    __syncthreads();
+    const uint32_t cand_total = s_ncand;
+    int got = want;
+    if (cand_total <= (uint32_t)kSelRankMax) {
+        rank_candidates(cand_total, want, sh);
+    } else {
+        uint64_t key[kSelKpt];
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            const uint32_t idx = (uint32_t)(t + i * kSelThreads);
+            key[i] = (i < KPT && i < nv) ? (((uint64_t)u[i] << 32) | (uint64_t)(~idx)) : 0ull;
+        }
+        got = select_block(key, k, sh);
+    }
+
+    // ---- output, best first ----
+    for (int i = t; i < got; i += kSelThreads) {
+        const uint64_t me = sh.sel[i];
+        out_ids[(int64_t)q * k + i] = (int32_t)key_id(me);
+        if (out_scores) out_scores[(int64_t)q * k + i] = key_score(me);
+    }
+}
+
 // Final ranking of the filtered matrix-core scan, one block per query. The
 // candidates of query q are the k keys of the sample, `first[q][0 .. k)`,
 // then the survivors of every scan block g, regions[q][g][0 .. counts[q][g]).
@@ -792,6 +990,22 @@ hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, i
     dim3 grid((unsigned)nchunks, (unsigned)nq);
     hipLaunchKernelGGL((select_kernel<true>), grid, dim3(kSelThreads), 0, st, scores,
                        (const uint64_t*)nullptr, n, k, nchunks, cand, out_ids, out_scores);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, int32_t* out_ids,
+                               float* out_scores, hipStream_t st) {
+    const int64_t kpt = (n + kSelThreads - 1) / kSelThreads;
+    dim3 grid(1u, (unsigned)nq);
+#define IS_SELECT_SMALL(KPT)                                                                      \
+    hipLaunchKernelGGL((select_small_kernel<KPT>), grid, dim3(kSelThreads), 0, st, scores, n, k,  \
+                       out_ids, out_scores)
+    if (kpt <= 4) IS_SELECT_SMALL(4);
+    else if (kpt <= 8) IS_SELECT_SMALL(8);
+    else if (kpt <= 12) IS_SELECT_SMALL(12);
+    else if (kpt <= 16) IS_SELECT_SMALL(16);
+    else return hipErrorInvalidValue;
+#undef IS_SELECT_SMALL
     return hipGetLastError();
 }
 

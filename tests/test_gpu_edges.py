@@ -76,6 +76,31 @@ def test_retrieve_exact_ties_go_to_lower_id():
     assert buf.ids[0, :5].tolist() == [3, 5, 9, 3000, 3999]
 
 
+@pytest.mark.parametrize("n,k", [(3000, 10), (16384, 40), (700, 700)])
+def test_retrieve_many_tied_scores(n, k):
+    # a few rows above a block of thousands of exactly tied rows: more tied
+    # candidates than the pairwise ranking takes, so the single-chunk select
+    # falls back to its general radix path; ties go to the lower id
+    d = 16
+    bank = torch.zeros(n, d, device="cuda")
+    bank[:, 0] = 0.25
+    top = {7: 0.75, n // 2: 0.5, n - 1: 0.5, 100: 0.625, 3: 1.0}
+    for j, v in top.items():
+        bank[j, 0] = v
+    q = torch.zeros(1, d, device="cuda")
+    q[0, 0] = 1.0
+    buf = RequestBuffers(n=n, d=d, k=k, nq=1, emb_dtype=torch.float32, max_tokens=1)
+    buf.retrieve(q, bank)
+    torch.cuda.synchronize()
+    ranked = sorted(range(n), key=lambda j: (-top.get(j, 0.25), j))[:k]
+    assert buf.ids[0].tolist() == ranked
+    qh, odt = host_emb(q)
+    bh, _ = host_emb(bank)
+    ids_o, _, _ = oracle.retrieve(qh, bh, n, d, k, 1, 0, odt)
+    assert buf.ids[0].tolist() == ids_o[0].tolist()
+    assert buf.scores[0].tolist() == [top.get(j, 0.25) for j in ranked]
+
+
 def test_retrieve_exact_ties_matrix_core_path():
     w = _ret_case(5000, 256, 8, 64, "bf16", True, seed=2)
     bank = workloads.make_bank(w, "cuda")
