@@ -210,6 +210,28 @@ def test_place_inject_shapes(H, D, L, P, start, lo, hi, k, rev):
     log(f"H={H} D={D} L={L} P={P} start={start} rev={rev}: floor-rescued {floor}")
 
 
+def test_place_inject_largest_k():
+    # k = IS_MAX_K facts: every thread of the inject workgroup owns one fact
+    # of the placement prefix; zero-length facts mixed in
+    w = workloads.TINY.with_(L=2, n=2000, k=1024, len_lo=0, len_hi=3, index=71)
+    inst = Instance(w)
+    inst.run()
+    inst.check_slot_map()
+    floor = inst.check_inject_full()
+    log(f"k=1024: m={int(inst.buf.m[0])}, floor-rescued {floor}")
+
+
+def test_place_inject_more_requests_than_cus():
+    # 300 requests in one slot-map and one inject launch: one inject
+    # workgroup per request, more workgroups than CUs
+    w = workloads.TINY.with_(L=2, nq=300, n=200, k=3, len_lo=1, len_hi=5, index=72)
+    inst = Instance(w)
+    inst.run()
+    inst.check_slot_map()
+    floor = inst.check_inject_full()
+    log(f"nq=300: m total={int(inst.buf.m.sum())}, floor-rescued {floor}")
+
+
 def _small_setup(max_tokens=64, max_blocks=8):
     w = workloads.TINY.with_(L=2, n=50, k=4, len_lo=2, len_hi=6, index=55)
     inst = Instance(w, max_tokens=max_tokens)
