@@ -791,25 +791,38 @@ __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
         uint32_t tm = 0;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) tm = (i < nv && u[i] > tm) ? u[i] : tm;
-        // holders: the min(M, kSelThreads) >= want threads with a valid key
+        // holders: the min(M, kSelThreads) >= want threads with a valid key.
+        // Maxima of non-negative scores (top bit set) are bracketed on their
+        // own when there are at least `want` of them, so that a single
+        // negative maximum does not widen the first radix window to the sign
+        const bool nonneg = nv > 0 && (tm & 0x80000000u) != 0;
         const uint32_t wmax = wave_max_u32(tm);
         const uint32_t wmin = wave_min_u32(nv > 0 ? tm : 0xFFFFFFFFu);
+        const uint32_t wmin_nn = wave_min_u32(nonneg ? tm : 0xFFFFFFFFu);
+        const uint32_t wnn = (uint32_t)__popcll(__ballot(nonneg));
         if (lane == 0) {
             sh.group[wave] = wmax;
             sh.group[kSelWaves + wave] = wmin;
+            sh.group[2 * kSelWaves + wave] = wmin_nn;
+            sh.group[3 * kSelWaves + wave] = wnn;
         }
         if (t < 256) {
             sh.hist[t] = 0;
             s_hist2[t] = 0;
         }
         __syncthreads();
-        uint32_t ref = 0, lowest = 0xFFFFFFFFu;
+        uint32_t ref = 0, lowest = 0xFFFFFFFFu, lowest_nn = 0xFFFFFFFFu, n_nn = 0;
 #pragma unroll
         for (int w = 0; w < kSelWaves; ++w) {
             ref = max(ref, (uint32_t)sh.group[w]);
             lowest = min(lowest, (uint32_t)sh.group[kSelWaves + w]);
+            lowest_nn = min(lowest_nn, (uint32_t)sh.group[2 * kSelWaves + w]);
+            n_nn += (uint32_t)sh.group[3 * kSelWaves + w];
         }
-        const uint32_t diff = ref ^ lowest;  // every holder's maximum lies in [lowest, ref]
+        if (n_nn >= (uint32_t)want) lowest = lowest_nn;
+        // at least `want` maxima lie in [lowest, ref]; those below are left
+        // out of the histogram by the prefix test
+        const uint32_t diff = ref ^ lowest;
         if (diff == 0) {
             tau = ref;
         } else {
