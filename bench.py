@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--detail", action="store_true",
                     help="also time one stream (latency) and each call separately")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip timing each step alone after evicting the caches (1 GiB of writes)")
     ap.add_argument("--store", default="device", choices=["device", "host"],
                     help="where the pre-RoPE K/V store lives: HBM, or pinned host memory "
                          "that the inject kernel reads over PCIe")
@@ -319,6 +321,25 @@ def main():
         latency_ms = timed(1) / args.steps
         log(f"one stream: {latency_ms * 1e3:.1f} us/step")
 
+    # ---- cold caches: each step alone after 1 GiB of writes (untimed) -------
+    # evicts the bank, the placement arrays and any page lines from the
+    # 256 MB Infinity Cache and the L2s; events bracket the step only
+    cold_ms = None
+    if not args.no_cold and nwaves == 1:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cold = []
+        for i in range(args.warmup, nsteps):
+            flush.fill_(i & 0xFF)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            step(i)
+            b.record()
+            torch.cuda.synchronize()
+            cold.append(a.elapsed_time(b))
+        del flush
+        cold_ms = statistics.median(cold)
+        log(f"cold caches: median {cold_ms * 1e3:.1f} us/step")
+
     # ---- instrumented pass (--detail): per-call events, one stream --------------
     per = {"retrieve": [], "slot_map": [], "inject": [], "step": []}
     recs = []
@@ -443,6 +464,7 @@ def main():
         "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
                         if args.detail else None),
         "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
+        "cold_cache_us_per_step_median": None if cold_ms is None else round(cold_ms * 1e3, 2),
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),
         "retrieve": None if ret_ms is None or ann is not None else {
