@@ -119,8 +119,10 @@ def main():
     bts = bts.view(R, wave, -1)
     pk, pv, num_slots = workloads.make_pages(w, num_blocks, dev)
     S = max(1, args.streams)
+    # a second buffer set and stream for the two-stream throughput figure
+    S_pool = max(S, 2) if (nwaves == 1 and R % 2 == 0) else S
     bufs = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
-                           max_tokens=w.max_tokens, device=dev) for _ in range(S)]
+                           max_tokens=w.max_tokens, device=dev) for _ in range(S_pool)]
     buf = bufs[0]
     ann = None
     if args.retriever == "ann":
@@ -193,7 +195,7 @@ def main():
             inject(j, b)
 
     main_stream = torch.cuda.current_stream()
-    streams = [main_stream] + [torch.cuda.Stream() for _ in range(S - 1)]
+    streams = [main_stream] + [torch.cuda.Stream() for _ in range(S_pool - 1)]
 
     def timed(nstreams):
         """K steps spread round robin over nstreams streams, bracketed by
@@ -225,6 +227,12 @@ def main():
     ms_per_step = total_ms / args.steps
     log(f"timed {args.steps} steps over {S} stream(s): {total_ms:.3f} ms GPU "
         f"({wall * 1e3:.3f} ms host wall)")
+    # throughput with two requests in flight (requests alternate between two
+    # streams, each with its own buffers and page regions)
+    two_ms = None
+    if S == 1 and S_pool >= 2:
+        two_ms = timed(2) / args.steps
+        log(f"two streams: {two_ms * 1e3 / w.nq:.1f} us per request")
 
     # ---- inject kernel alone: the same K requests' injects back to back -------
     # (their retrieval and slot maps are recomputed untimed into one buffer
@@ -460,6 +468,8 @@ def main():
                       if host_store else "HBM"),
         },
         "streams": S,
+        "throughput_2_streams_us_per_request": (None if two_ms is None
+                                                else round(two_ms * 1e3 / w.nq, 3)),
         "inject_launch_us": round(inj_launch_ms * 1e3, 2),
         "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
                         if args.detail else None),
