@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     __shared__ int64_t s_wave_tot[kInjThreads / kWave];
     __shared__ uint32_t s_flags;
     __shared__ int32_t s_bad;
-    __shared__ int32_t s_next;                // next work item of the share
+    __shared__ int32_t s_next;                // next work item of this workgroup
 
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r = blockIdx.y;
