@@ -110,14 +110,16 @@ def main():
     nwaves = w.nq // wave
 
     t0 = time.time()
-    bank = workloads.make_bank(w, dev)
-    store = workloads.make_store(w, dev, host=host_store)
-    queries = torch.stack([workloads.make_queries(w, dev, variant=i) for i in range(nsteps)])
+    # the paged cache is allocated first, as an engine allocates its KV cache
+    # at start-up before a memory store fills up
     region_bytes = 2 * int(1.1 * wave * w.max_blocks) * w.page_size * w.L * w.H * w.D * 2
     R = max(1, min(8, int(60e9 // region_bytes)))
     bts, num_blocks = workloads.make_block_tables(w.with_(nq=R * wave), dev, variant=0)
     bts = bts.view(R, wave, -1)
     pk, pv, num_slots = workloads.make_pages(w, num_blocks, dev)
+    bank = workloads.make_bank(w, dev)
+    store = workloads.make_store(w, dev, host=host_store)
+    queries = torch.stack([workloads.make_queries(w, dev, variant=i) for i in range(nsteps)])
     S = max(1, args.streams)
     # a second buffer set and stream for the two-stream throughput figure
     S_pool = max(S, 2) if (nwaves == 1 and R % 2 == 0) else S
