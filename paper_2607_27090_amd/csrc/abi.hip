@@ -1,6 +1,7 @@
 // C ABI of libinferscale: host-side argument validation, workspace layout and
 // launch sequencing. The contract of every entry point is documented in
 // include/inferscale.h.
+#include <atomic>
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
@@ -262,17 +263,18 @@ int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dt
 namespace is {
 
 int compute_units() {
-    static int cached[64] = {0};
+    // cached per device; threads racing on the first call store the same value
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int cus = 0;
+    int cus = cached[dev].load(std::memory_order_relaxed);
+    if (cus == 0) {
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             cus <= 0)
             cus = 256;
-        cached[dev] = cus;
+        cached[dev].store(cus, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return cus;
 }
 
 }  // namespace is

@@ -31,6 +31,8 @@
 //     computed while its loads are in flight;
 //   * loads and stores are non-temporal: every stored byte is read once and
 //     every page byte is written once.
+#include <atomic>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -299,9 +301,12 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     if (per_req > items_max) per_req = items_max;
     if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
-    static bool lds_attr_set[64] = {false};
+    // allow the dynamic LDS reserve (once per device; setting it twice from
+    // racing threads is harmless)
+    static std::atomic<bool> lds_attr_set[64];
     int dev = 0;
-    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 &&
+        !lds_attr_set[dev].load(std::memory_order_acquire)) {
         hipError_t e = hipFuncSetAttribute((const void*)inject_kernel<false>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)kInjLdsReserve);
@@ -310,7 +315,7 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                                     hipFuncAttributeMaxDynamicSharedMemorySize,
                                     (int)kInjLdsReserve);
         if (e != hipSuccess) return e;
-        lds_attr_set[dev] = true;
+        lds_attr_set[dev].store(true, std::memory_order_release);
     }
     if (interleaved)
         hipLaunchKernelGGL(inject_kernel<true>, grid, dim3(kInjThreads), kInjLdsReserve, st, ids,
