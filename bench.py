@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--detail", action="store_true",
                     help="also time one stream (latency) and each call separately")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
+    ap.add_argument("--no-two-streams", action="store_true",
+                    help="skip the two-stream throughput figure (its kernels overlap, which "
+                         "per-kernel profiles should not average in)")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip timing each step alone after evicting the caches (1 GiB of writes)")
     ap.add_argument("--store", default="device", choices=["device", "host"],
@@ -122,7 +125,7 @@ def main():
     queries = torch.stack([workloads.make_queries(w, dev, variant=i) for i in range(nsteps)])
     S = max(1, args.streams)
     # a second buffer set and stream for the two-stream throughput figure
-    S_pool = max(S, 2) if (nwaves == 1 and R % 2 == 0) else S
+    S_pool = max(S, 2) if (nwaves == 1 and R % 2 == 0 and not args.no_two_streams) else S
     bufs = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
                            max_tokens=w.max_tokens, device=dev) for _ in range(S_pool)]
     buf = bufs[0]
@@ -222,6 +225,12 @@ def main():
     for i in range(args.warmup):
         with torch.cuda.stream(streams[i % S]):
             step(i, bufs[i % S])
+    # the extra stream and buffer set of the two-stream figure are warmed up
+    # too (a stream's first launches carry one-time queue set-up)
+    for si in range(S, S_pool):
+        for i in range(2):
+            with torch.cuda.stream(streams[si]):
+                step(i, bufs[si])
     torch.cuda.synchronize()
     t_host = time.perf_counter()
     total_ms = timed(S)
