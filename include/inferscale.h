@@ -187,6 +187,10 @@ int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
  *   D              head dimension: a multiple of 16, <= IS_MAX_HEAD_DIM
  * Tokens whose slot lies outside [0, num_slots) and facts whose rows fall
  * outside the store are skipped and flagged.
+ * Launch footprint: max(1, CUs / nq) workgroups of 1024 threads per request,
+ * each reserving 84 KiB of LDS so that it has its CU to itself; kernels on
+ * other streams can share those CUs only within the remaining LDS and
+ * registers.
  */
 int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
               const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
