@@ -44,9 +44,11 @@ class Instance:
         self.buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=self.bank.dtype,
                                   max_tokens=self.max_tokens, device=device)
 
-    def run(self, reverse_rank=1, inv_freq=None, interleaved=False):
+    def run(self, reverse_rank=1, inv_freq=None, interleaved=False, stream=None, sync=True):
         """One pass; inv_freq (float64 numpy [D/2]) and interleaved select the
-        rotary table and pair layout (kept for the checks)."""
+        rotary table and pair layout (kept for the checks). ``stream`` (a
+        torch stream, default the current one) takes the three calls; with
+        ``sync=False`` the pass is left in flight."""
         from paper_2607_27090_amd import IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED
         w = self.w
         self.inv_freq, self.interleaved = inv_freq, bool(interleaved)
@@ -55,8 +57,10 @@ class Instance:
         run_request(self.buf, self.query, self.bank, self.store, self.bt, self.pk, self.pv,
                     start_pos=w.start_pos, page_size=w.page_size, rope_theta=w.theta,
                     shared_bank=w.shared_bank, reverse_rank=reverse_rank, inv_freq=tf,
-                    pairing=IS_ROPE_INTERLEAVED if interleaved else IS_ROPE_HALF_SPLIT)
-        torch.cuda.synchronize()
+                    pairing=IS_ROPE_INTERLEAVED if interleaved else IS_ROPE_HALF_SPLIT,
+                    stream=stream)
+        if sync:
+            torch.cuda.synchronize()
 
     # ---- checks --------------------------------------------------------------
 
@@ -101,8 +105,10 @@ class Instance:
         self._place = o
         return o
 
-    def check_inject_full(self):
-        """Oracle inject into host pools of the same size; compare everything."""
+    def check_inject_full(self, foreign_slots=None):
+        """Oracle inject into host pools of the same size; compare everything.
+        ``foreign_slots`` are slots of the same pool that other requests wrote
+        (left out of the check that nothing outside the placement changed)."""
         w = self.w
         o = self._place
         L, T, H, D = self.store["preK"].shape
@@ -134,12 +140,17 @@ class Instance:
                            interleaved=getattr(self, "interleaved", False))
         assert st == 0
         gk, gv = u16(self.pk), u16(self.pv)
-        assert np.array_equal(gv, hv), "V pages differ"
+        own = np.ones(self.num_slots, dtype=bool)
+        if foreign_slots is not None:
+            own[np.asarray(foreign_slots, dtype=np.int64)] = False
+        assert np.array_equal(gv[:, own], hv[:, own]), "V pages differ"
         same = gk == hk
         touched = np.zeros(self.num_slots, dtype=bool)
         for r in range(w.nq):
             touched[o["slots"][r, :o["m"][r]]] = True
-        assert same[:, ~touched].all(), "a slot outside the placement was written"
+        assert not (touched & ~own).any(), "own and foreign slots overlap"
+        untouched = ~touched & own
+        assert same[:, untouched].all(), "a slot outside the placement was written"
         pre = np.empty((L, self.num_slots, H, D), dtype=np.uint16)
         # unrotated inputs at each target slot, for the pair-norm floor
         for r in range(w.nq):
