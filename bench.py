@@ -78,6 +78,9 @@ def parse():
     ap.add_argument("--degree", type=int, default=64, help="ANN graph out-degree")
     ap.add_argument("--seeds", type=int, default=1024, help="ANN search entry points")
     ap.add_argument("--max-iters", type=int, default=512)
+    ap.add_argument("--path", default="fused", choices=["fused", "separate"],
+                    help="fused: retrieve, then one place + inject launch; separate: retrieve, "
+                         "slot map, inject (the other path is timed too and reported beside)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
@@ -93,7 +96,8 @@ def main():
     import torch
     import workloads
     from paper_2607_27090_amd import (IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED, is_inject,
-                                      is_inject_rotary, is_paged_scores, is_slot_map)
+                                      is_inject_rotary, is_paged_scores, is_place_inject,
+                                      is_slot_map)
     from paper_2607_27090_amd.pipeline import AnnIndex, RequestBuffers
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -174,6 +178,8 @@ def main():
     rope_table = None
     if args.rope == "llama3.1":
         rope_table = torch.from_numpy(workloads.llama31_inv_freq(w.D, w.theta)).to(dev)
+    pairing = IS_ROPE_INTERLEAVED if args.rope == "interleaved" else IS_ROPE_HALF_SPLIT
+    fused = args.path == "fused"
 
     def inject(j, b=None):
         b = buf if b is None else b
@@ -188,21 +194,39 @@ def main():
                       w.theta, pk, pv, **kw)
         else:
             is_inject_rotary(b.ids[sl], store["preK"], store["V"], b.slots[sl], b.positions[sl],
-                             w.theta, pk, pv, inv_freq=rope_table,
-                             pairing=(IS_ROPE_INTERLEAVED if args.rope == "interleaved"
-                                      else IS_ROPE_HALF_SPLIT), **kw)
+                             w.theta, pk, pv, inv_freq=rope_table, pairing=pairing, **kw)
 
-    def step(i, b=None):
+    def place_inject(i, j, b=None):
+        b = buf if b is None else b
+        sl = slice(j * wave, (j + 1) * wave)
+        ls = lens if lens_stride == 0 else lens[sl]
+        os_ = offs if lens_stride == 0 else offs[sl]
+        is_place_inject(b.ids[sl], store["preK"], store["V"], w.theta, pk, pv, b.slots[sl],
+                        b.positions[sl], b.m[sl], fact_offsets=os_, fact_lens=ls,
+                        start_pos=w.start_pos, block_table=bts[(i * nwaves + j) % R],
+                        page_size=w.page_size, max_blocks=bts.shape[-1], k=w.k, nq=wave, n=w.n,
+                        lens_stride=lens_stride, max_tokens=w.max_tokens, L=L, H=H, D=D,
+                        T_store=T, num_slots=num_slots, inv_freq=rope_table, pairing=pairing,
+                        status=b.status)
+
+    def after_retrieve(i, b=None, use_fused=None):
+        """Placement and injection of step i's requests."""
+        for j in range(nwaves):
+            if fused if use_fused is None else use_fused:
+                place_inject(i, j, b)
+            else:
+                place(i, j, b)
+                inject(j, b)
+
+    def step(i, b=None, use_fused=None):
         b = buf if b is None else b
         retrieve(queries[i], b)
-        for j in range(nwaves):
-            place(i, j, b)
-            inject(j, b)
+        after_retrieve(i, b, use_fused)
 
     main_stream = torch.cuda.current_stream()
     streams = [main_stream] + [torch.cuda.Stream() for _ in range(S_pool - 1)]
 
-    def timed(nstreams):
+    def timed(nstreams, use_fused=None):
         """K steps spread round robin over nstreams streams, bracketed by
         events on the main stream that every other stream waits on and is
         waited for."""
@@ -214,7 +238,7 @@ def main():
         for i in range(args.warmup, nsteps):
             si = (i - args.warmup) % nstreams
             with torch.cuda.stream(streams[si]):
-                step(i, bufs[si])
+                step(i, bufs[si], use_fused)
         for s_ in streams[1:nstreams]:
             main_stream.wait_stream(s_)
         ev1.record(main_stream)
@@ -244,10 +268,18 @@ def main():
     if S == 1 and S_pool >= 2:
         two_ms = timed(2) / args.steps
         log(f"two streams: {two_ms * 1e3 / w.nq:.1f} us per request")
+    # the other path (separate slot map + inject, or the fused launch), same
+    # steps, one stream, after its own warm-up
+    for i in range(2):
+        step(i, buf, not fused)
+    other_ms = timed(S, not fused) / args.steps
+    log(f"{'separate calls' if fused else 'fused place + inject'}: "
+        f"{other_ms * 1e3 / w.nq:.1f} us per request")
 
     # ---- inject kernel alone: the same K requests' injects back to back -------
-    # (their retrieval and slot maps are recomputed untimed into one buffer
-    # set per step, so only inject launches sit between the two events)
+    # (their retrieval -- and, on the separate path, slot maps -- are
+    # recomputed untimed into one buffer set per step, so only inject (or
+    # place + inject) launches sit between the two events)
     sets = [RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=bank.dtype,
                            max_tokens=w.max_tokens, device=dev, workspace=buf.workspace)
             for _ in range(args.steps)]
@@ -256,14 +288,18 @@ def main():
             sets[si].ann_iters = torch.zeros(w.nq, dtype=torch.int32, device=dev)
             sets[si].ann_scored = torch.zeros(w.nq, dtype=torch.int32, device=dev)
         retrieve(queries[i], sets[si])
-        for j in range(nwaves):
-            place(i, j, sets[si])
+        if not fused:
+            for j in range(nwaves):
+                place(i, j, sets[si])
     torch.cuda.synchronize()
     ei0, ei1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ei0.record()
-    for si in range(args.steps):
+    for si, i in enumerate(range(args.warmup, nsteps)):
         for j in range(nwaves):
-            inject(j, sets[si])
+            if fused:
+                place_inject(i, j, sets[si])
+            else:
+                inject(j, sets[si])
     ei1.record()
     torch.cuda.synchronize()
     inj_launch_ms = ei0.elapsed_time(ei1) / (args.steps * nwaves)
@@ -361,6 +397,8 @@ def main():
 
     # ---- instrumented pass (--detail): per-call events, one stream --------------
     per = {"retrieve": [], "slot_map": [], "inject": [], "step": []}
+    if fused:
+        per = {"retrieve": [], "place_inject": [], "step": []}
     recs = []
     for i in (range(args.warmup, nsteps) if args.detail else ()):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * nwaves)]
@@ -368,9 +406,13 @@ def main():
         retrieve(queries[i], buf)
         e[1].record()
         for j in range(nwaves):
-            place(i, j)
-            e[2 + 2 * j].record()
-            inject(j)
+            if fused:
+                e[2 + 2 * j].record()
+                place_inject(i, j)
+            else:
+                place(i, j)
+                e[2 + 2 * j].record()
+                inject(j)
             e[3 + 2 * j].record()
         recs.append(e)
     torch.cuda.synchronize()
@@ -381,13 +423,19 @@ def main():
             sm += prev.elapsed_time(e[2 + 2 * j])
             inj += e[2 + 2 * j].elapsed_time(e[3 + 2 * j])
             prev = e[3 + 2 * j]
-        per["slot_map"].append(sm)
-        per["inject"].append(inj)
+        if fused:
+            per["place_inject"].append(inj)
+        else:
+            per["slot_map"].append(sm)
+            per["inject"].append(inj)
         per["step"].append(e[0].elapsed_time(e[-1]))
     # placed tokens per step
     m_steps = [int(b.m.sum()) for b in sets]
     assert all(int(b.status.item()) == 0 for b in sets + bufs), "device status flags raised"
     inj_bytes = [workloads.inject_algorithmic_bytes(w, m) for m in m_steps]
+    if fused:
+        # the fused launch also writes each placed token's slot and position
+        inj_bytes = [b_ + 12 * m for b_, m in zip(inj_bytes, m_steps)]
     # algorithmic bytes per inject launch / mean launch duration (timed region)
     achieved = statistics.fmean(inj_bytes) / nwaves / (inj_launch_ms * 1e-3) / 1e9
     ret_ms = statistics.fmean(per["retrieve"]) if per["retrieve"] else None
@@ -407,14 +455,12 @@ def main():
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
             retrieve(qbuf, buf)
-            place(0, 0)
-            inject(0)
+            after_retrieve(0, buf)
         torch.cuda.current_stream().wait_stream(s)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             retrieve(qbuf, buf)
-            place(0, 0)
-            inject(0)
+            after_retrieve(0, buf)
         torch.cuda.synchronize()
         times = []
         for i in range(args.warmup, nsteps):
@@ -478,6 +524,10 @@ def main():
                       f"({w.payloads} payloads, {2 * store['preK'].numel() * 2 / 1e9:.1f} GB)"
                       if host_store else "HBM"),
         },
+        "path": ("retrieve, then placement + slot map + inject in one launch" if fused
+                 else "retrieve, slot map, inject (three calls)"),
+        ("separate_calls_us_per_request" if fused else "fused_us_per_request"):
+            round(other_ms * 1e3 / w.nq, 3),
         "streams": S,
         "throughput_2_streams_us_per_request": (None if two_ms is None
                                                 else round(two_ms * 1e3 / w.nq, 3)),
@@ -497,18 +547,19 @@ def main():
         "ann": ann,
         "roofline": {
             "bound": "hbm",
-            "kernel": "inject_kernel",
+            "kernel": "inject_kernel (place + inject)" if fused else "inject_kernel",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic() if args.workload == "llama8b" and w.k == 50 else None,
+            "traffic": (measured_traffic(fused) if args.workload == "llama8b" and w.k == 50
+                        and args.rope == "default" else None),
             "traffic_unit": "HBM bytes per launch (scaled FETCH_SIZE + WRITE_SIZE)",
             "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves),
         } if not host_store else {
             # the store half of the inject traffic crosses the host link
             "bound": "pcie",
-            "kernel": "inject_kernel",
+            "kernel": "inject_kernel (place + inject)" if fused else "inject_kernel",
             "achieved": round(achieved / 2, 1),
             "peak": PCIE_PEAK_GBPS,
             "unit": "GB/s",
@@ -521,12 +572,14 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def measured_traffic():
-    """HBM bytes per inject launch from the committed counter summary, or
-    None when the kernel sources changed since the counters were taken."""
+def measured_traffic(fused):
+    """HBM bytes per inject launch from the committed counter summary of the
+    path timed, or None when the kernel sources changed since the counters
+    were taken."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "inject_kernel_llama8b_k50_traffic.md")
+    name = "place_inject" if fused else "inject_kernel"
+    path = os.path.join(ROOT, "profiles", f"{name}_llama8b_k50_traffic.md")
     csrc = os.path.join(ROOT, "paper_2607_27090_amd", "csrc")
     try:
         text = open(path).read()

@@ -17,6 +17,8 @@
  *                rotates the key to the token's position (§3.3 composition;
  *                §2.4 and Theorem "Chunked RoPE Injection", §5.1) and writes
  *                both into the paged cache (§3.4).
+ * is_place_inject runs is_slot_map and is_inject as one launch, with the
+ * same results.
  *
  * Conventions shared by every call
  *   - All data pointers are DEVICE pointers owned by the caller. The library
@@ -226,6 +228,37 @@ int is_inject_rotary(const int32_t* ids, const void* preK, const void* V, const 
                      int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
                      int64_t num_slots, const double* inv_freq, int32_t pairing, uint32_t* status,
                      void* stream);
+
+/*
+ * is_place_inject -- is_slot_map and is_inject_rotary as one launch (§5.2
+ * placement and §2.2 slot mapping feeding the §3.4 injection; §3.3 and §5.1
+ * rotation).
+ *
+ * For every request it computes exactly what is_slot_map followed by
+ * is_inject_rotary computes: out_slots, out_positions and out_m as
+ * is_slot_map writes them, and the same page contents and status flags.
+ * The injection's set-up forms the placement offsets anyway, so each
+ * token's slot is taken from the block table directly and the slot map's
+ * separate launch (and its round trip through memory) is saved.
+ *
+ * Arguments: those of is_slot_map (start_pos, block_table, page_size,
+ * max_blocks, out_slots, out_positions, out_m) and of is_inject_rotary
+ * (the store, pages, rotary table and pair layout), with the same meaning,
+ * layout, alignment and ownership; k, nq (<= 65535), n, lens_stride,
+ * reverse_rank and max_tokens are shared. A request that is_slot_map would
+ * skip (an id out of range, a negative length, more than max_tokens tokens,
+ * positions beyond its block table, a negative block it uses) gets m = 0 and
+ * no page is written for it; flags as for the two calls together.
+ * Launch footprint: as is_inject's.
+ */
+int is_place_inject(const int32_t* ids, const void* preK, const void* V,
+                    const int64_t* fact_offsets, const int32_t* fact_lens, int32_t start_pos,
+                    const int32_t* block_table, int32_t page_size, int32_t max_blocks,
+                    float rope_theta, const double* inv_freq, int32_t pairing, void* paged_k,
+                    void* paged_v, int64_t* out_slots, int32_t* out_positions, int32_t* out_m,
+                    int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+                    int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+                    int64_t num_slots, uint32_t* status, void* stream);
 
 /*
  * is_paged_scores -- the consumer of the injected pages: attention logits of

@@ -45,7 +45,7 @@ IS_ANN_MAX_WIDTH = 4
 IS_ANN_MAX_EXPAND = 256
 
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_slot_map", "is_inject", "is_inject_rotary", "is_paged_scores",
+            "is_slot_map", "is_inject", "is_inject_rotary", "is_place_inject", "is_paged_scores",
             "is_ann_build_workspace_size", "is_ann_build", "is_ann_search_workspace_size",
             "is_ann_search")
 
@@ -86,6 +86,9 @@ def load_library() -> ctypes.CDLL:
     lib.is_inject_rotary.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32,
                                      i32, i32, i32, i32, i64, i64, P, i32, P, P]
     lib.is_inject_rotary.restype = ctypes.c_int
+    lib.is_place_inject.argtypes = [P, P, P, P, P, i32, P, i32, i32, f32, P, i32, P, P, P, P, P,
+                                    i32, i32, i64, i64, i32, i32, i32, i32, i32, i64, i64, P, P]
+    lib.is_place_inject.restype = ctypes.c_int
     lib.is_paged_scores.argtypes = [P, P, P, i32, P, i32, i32, P, P, i32, i32, i32, i32, i32,
                                     i64, i32, i32, f32, P, i32, P, P]
     lib.is_paged_scores.restype = ctypes.c_int
@@ -219,6 +222,21 @@ def is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_
         float(rope_theta), _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens),
         _ptr(m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
         _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
+
+
+def is_place_inject(ids, preK, V, rope_theta, paged_k, paged_v, out_slots, out_positions, out_m,
+                    *, fact_offsets, fact_lens, start_pos, block_table, page_size, max_blocks, k,
+                    nq, n, lens_stride, reverse_rank=1, max_tokens, L, H, D, T_store, num_slots,
+                    inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
+    """Slot map + inject in one launch (see include/inferscale.h)."""
+    if inv_freq is not None and inv_freq.dtype != torch.float64:
+        raise ValueError("inv_freq must be a float64 tensor")
+    _check("is_place_inject", load_library().is_place_inject(
+        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(fact_offsets), _ptr(fact_lens),
+        start_pos, _ptr(block_table), page_size, max_blocks, float(rope_theta), _ptr(inv_freq),
+        int(pairing), _ptr(paged_k), _ptr(paged_v), _ptr(out_slots), _ptr(out_positions),
+        _ptr(out_m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store,
+        num_slots, _ptr(status), _stream(stream)))
 
 
 def is_paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, m, scores, *,

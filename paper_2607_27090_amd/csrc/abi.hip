@@ -407,6 +407,59 @@ int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t
                             status, stream);
 }
 
+int is_place_inject(const int32_t* ids, const void* preK, const void* V,
+                    const int64_t* fact_offsets, const int32_t* fact_lens, int32_t start_pos,
+                    const int32_t* block_table, int32_t page_size, int32_t max_blocks,
+                    float rope_theta, const double* inv_freq, int32_t pairing, void* paged_k,
+                    void* paged_v, int64_t* out_slots, int32_t* out_positions, int32_t* out_m,
+                    int32_t k, int32_t nq, int64_t n, int64_t lens_stride, int32_t reverse_rank,
+                    int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
+                    int64_t num_slots, uint32_t* status, void* stream) {
+    if (!ids || !preK || !V || !fact_offsets || !fact_lens || !block_table || !paged_k ||
+        !paged_v || !out_slots || !out_positions || !out_m)
+        return fail(IS_ERR_INVALID, "every array argument except status and inv_freq must be non-NULL");
+    if (k < 1 || k > IS_MAX_K) return fail(IS_ERR_INVALID, "k=%d must be in [1, %d]", k, IS_MAX_K);
+    if (nq < 1 || nq > 65535) return fail(IS_ERR_INVALID, "nq=%d must be in [1, 65535]", nq);
+    if (n < 1 || n > INT32_MAX) return fail(IS_ERR_INVALID, "n=%lld must be in [1, 2^31)", (long long)n);
+    if (page_size < 1) return fail(IS_ERR_INVALID, "page_size=%d must be >= 1", page_size);
+    if (start_pos < 0) return fail(IS_ERR_INVALID, "start_pos=%d must be >= 0", start_pos);
+    if (max_blocks < 0 || max_tokens < 0)
+        return fail(IS_ERR_INVALID, "max_blocks and max_tokens must be >= 0");
+    if ((int64_t)start_pos + max_tokens > INT32_MAX)
+        return fail(IS_ERR_INVALID, "start_pos + max_tokens must stay below 2^31");
+    if (L < 1 || H < 1) return fail(IS_ERR_INVALID, "L=%d and H=%d must be >= 1", L, H);
+    if (D < 16 || D % 16 || D > IS_MAX_HEAD_DIM)
+        return fail(IS_ERR_UNSUPPORTED, "D=%d must be a multiple of 16 in [16, %d]", D,
+                    IS_MAX_HEAD_DIM);
+    if ((int64_t)H * D > (1 << 20)) return fail(IS_ERR_UNSUPPORTED, "H*D=%lld too large", (long long)H * D);
+    if (T_store < 0 || num_slots < 0 || lens_stride < 0)
+        return fail(IS_ERR_INVALID, "T_store, num_slots and lens_stride must be >= 0");
+    if (!inv_freq && (!(rope_theta > 0.f) || !std::isfinite(rope_theta)))
+        return fail(IS_ERR_INVALID, "rope_theta must be positive and finite");
+    if (pairing != IS_ROPE_HALF_SPLIT && pairing != IS_ROPE_INTERLEAVED)
+        return fail(IS_ERR_INVALID, "pairing=%d is neither IS_ROPE_HALF_SPLIT nor IS_ROPE_INTERLEAVED",
+                    pairing);
+    if (!aligned(preK, 16) || !aligned(V, 16) || !aligned(paged_k, 16) || !aligned(paged_v, 16))
+        return fail(IS_ERR_INVALID, "preK, V, paged_k and paged_v must be 16-byte aligned");
+    if (!aligned(out_slots, 8) || !aligned(fact_offsets, 8) || !aligned(ids, 4) ||
+        !aligned(out_positions, 4) || !aligned(fact_lens, 4) || !aligned(block_table, 4) ||
+        !aligned(out_m, 4) || (status && !aligned(status, 4)) ||
+        (inv_freq && !aligned(inv_freq, 8)))
+        return fail(IS_ERR_INVALID, "misaligned pointer argument");
+    int rc = check_store_pointer(preK, "preK");
+    if (rc) return rc;
+    rc = check_store_pointer(V, "V");
+    if (rc) return rc;
+    const is::PlaceArgs pl{block_table, out_slots, out_positions, out_m,
+                           start_pos, page_size, max_blocks};
+    hipError_t e = is::launch_inject(ids, preK, V, nullptr, nullptr, rope_theta, paged_k, paged_v,
+                                     fact_offsets, fact_lens, nullptr, k, nq, n, lens_stride,
+                                     reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+                                     inv_freq, pairing, status, (hipStream_t)stream, &pl);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "place + inject launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
 int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int32_t layer,
                     const int32_t* block_table, int32_t page_size, int32_t start_pos,
                     const int32_t* m, float* scores, int32_t nq, int32_t Hq, int32_t H, int32_t D,

@@ -31,6 +31,14 @@
 //     computed while its loads are in flight;
 //   * loads and stores are non-temporal: every stored byte is read once and
 //     every page byte is written once.
+//
+// The same kernel with PLACE set also does the placement and slot mapping
+// (§5.2 position policy, §2.2 block tables) itself: its set-up already
+// forms the placement offsets b_i, so a token's position is start_pos + idx
+// and its slot comes from the block table, the request is validated exactly
+// as the slot map validates it, and the slots, positions and m are written
+// as by-products. This saves the slot map's own launch on the request's
+// critical path.
 #include <atomic>
 
 #include "common.hpp"
@@ -43,6 +51,9 @@ constexpr int kInjLayers = 2;      // layers of one work item
 // dynamic LDS requested beyond the kernel's own, so that no two workgroups
 // share a CU (160 KiB of LDS per CU)
 constexpr size_t kInjLdsReserve = 84 * 1024;
+// block-table entries each thread loads with the fact ids (PLACE); blocks
+// beyond 2 * 1024 are read after the scan
+constexpr int kInjBtAhead = 2;
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -95,7 +106,9 @@ __device__ __forceinline__ void rotate8_interleaved(const uint4 lo, const uint4 
     out_hi = make_uint4(out[4], out[5], out[6], out[7]);
 }
 
-template <bool INTERLEAVED>
+// PLACE = false: slots, positions and m_dev are the slot map's outputs.
+// PLACE = true: they are not read; pl holds the block table and the outputs.
+template <bool INTERLEAVED, bool PLACE>
 __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     const int32_t* __restrict__ ids, const uint4* __restrict__ preK, const uint4* __restrict__ V,
     const int64_t* __restrict__ slots, const int32_t* __restrict__ positions, float rope_theta,
@@ -103,13 +116,16 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     const int64_t* __restrict__ fact_offsets, const int32_t* __restrict__ fact_lens,
     const int32_t* __restrict__ m_dev, int32_t k, int64_t n, int64_t lens_stride,
     int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D, int64_t T_store,
-    int64_t num_slots, const double* __restrict__ inv_freq, uint32_t* __restrict__ status) {
+    int64_t num_slots, const double* __restrict__ inv_freq, uint32_t* __restrict__ status,
+    PlaceArgs pl) {
     __shared__ int64_t s_b[IS_MAX_K + 1];     // placed-token offset of each fact
     __shared__ int64_t s_off[IS_MAX_K];       // store row of each fact, -1: skip
     __shared__ double s_invf[IS_MAX_HEAD_DIM / 2];
     __shared__ int64_t s_wave_tot[kInjThreads / kWave];
     __shared__ uint32_t s_flags;
     __shared__ int32_t s_bad;
+    __shared__ int32_t s_bad_block;           // PLACE: a used block-table entry is < 0
+    __shared__ int64_t s_first_neg;           // PLACE: lowest preloaded block whose entry is < 0
     __shared__ int32_t s_next;                // next work item of this workgroup
 
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -117,11 +133,25 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     // m and this thread's fact id (fact t of the placement order, k <= the
     // block size) are independent loads; the fact's length and store row
     // depend only on the id and are loaded together
-    const int32_t m_in = m_dev[r];
+    const int32_t m_in = PLACE ? 0 : m_dev[r];
     const int32_t* rid = ids + (int64_t)r * k;
     const int32_t cid = t < k ? (reverse_rank ? rid[k - 1 - t] : rid[t]) : 0;
-    const int32_t m = min(m_in, max_tokens);
-    if (m <= 0) return;
+    // PLACE: the block-table entries of the blocks the first placed tokens
+    // can use are independent of everything else and load now too
+    const int32_t* bt_r = PLACE ? pl.block_table + (int64_t)r * pl.max_blocks : nullptr;
+    const int64_t blk0 = PLACE ? pl.start_pos / pl.page_size : 0;
+    int32_t pb[kInjBtAhead] = {};
+    if (PLACE) {
+        const int64_t blk_cap =
+            max_tokens > 0 ? ((int64_t)pl.start_pos + max_tokens - 1) / pl.page_size : -1;
+#pragma unroll
+        for (int i = 0; i < kInjBtAhead; ++i) {
+            const int64_t b = blk0 + t + (int64_t)i * kInjThreads;
+            if (b <= blk_cap && b < pl.max_blocks) pb[i] = bt_r[b];
+        }
+    }
+    int32_t m = min(m_in, max_tokens);
+    if (!PLACE && m <= 0) return;
 
     // ---- per-request setup: placement offsets, store rows, frequencies ----
     const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
@@ -145,7 +175,10 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
         }
         s_off[t] = off;
     }
-    if (t == 0) { s_flags = 0; s_bad = 0; s_next = 0; }
+    if (t == 0) {
+        s_flags = 0; s_bad = 0; s_bad_block = 0; s_next = 0;
+        s_first_neg = INT64_MAX;
+    }
     const int64_t incl = wave_incl_scan(len, lane);
     if (lane == 63) s_wave_tot[wave] = incl;
     if (t < (D >> 1))
@@ -162,11 +195,56 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
         s_b[k] = tot;
     }
     if (t < k && (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN))) atomicOr(&s_flags, flags);
+    if (PLACE) {
+        // negative entries among the preloaded blocks; whether the placement
+        // reaches them is known once the total is
+#pragma unroll
+        for (int i = 0; i < kInjBtAhead; ++i)
+            if (pb[i] < 0)
+                atomicMin((unsigned long long*)&s_first_neg,
+                          (unsigned long long)(blk0 + t + (int64_t)i * kInjThreads));
+    }
     __syncthreads();
     if (s_bad) {
         // a request with an invalid id or length is skipped as a whole
-        if (blockIdx.x == 0 && t == 0 && status) atomicOr(status, s_flags);
+        if (blockIdx.x == 0 && t == 0) {
+            if (PLACE) pl.out_m[r] = 0;
+            if (status) atomicOr(status, s_flags);
+        }
         return;
+    }
+    if (PLACE) {
+        // the slot map's request checks, in its order: capacity, then a block
+        // table too short for the last position, then a negative block among
+        // those the placement uses; any of them skips the request (m = 0)
+        const int64_t total = s_b[k];
+        const int64_t blk_last = ((int64_t)pl.start_pos + total - 1) / pl.page_size;
+        uint32_t f = 0;
+        if (total > max_tokens) f = IS_DEV_CAPACITY;
+        else if (total > 0 && blk_last >= pl.max_blocks) f = IS_DEV_BT_SHORT;
+        if (f == 0 && total > 0) {
+            if (s_first_neg <= blk_last) f = IS_DEV_BAD_BLOCK;
+            const int64_t blk_more = blk0 + (int64_t)kInjBtAhead * kInjThreads;
+            if (f == 0 && blk_last >= blk_more) {
+                // blocks past the preloaded part: one more pass and barrier
+                bool bad = false;
+                for (int64_t b = blk_more + t; b <= blk_last; b += kInjThreads)
+                    if (bt_r[b] < 0) bad = true;
+                if (bad) s_bad_block = 1;
+                __syncthreads();
+                if (s_bad_block) f = IS_DEV_BAD_BLOCK;
+            }
+        }
+        if (f) {
+            if (blockIdx.x == 0 && t == 0) {
+                pl.out_m[r] = 0;
+                if (status) atomicOr(status, f);
+            }
+            return;
+        }
+        if (blockIdx.x == 0 && t == 0) pl.out_m[r] = (int32_t)total;
+        m = (int32_t)total;
+        if (m <= 0) return;
     }
     if (blockIdx.x != 0) flags = 0;  // fact-level flags are reported once per request
 
@@ -183,8 +261,10 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     // items: one front sweeping the request layer group by layer group
     const int64_t G = gridDim.x;
     const int64_t span = (total - blockIdx.x + G - 1) / G;
-    const int64_t* slots_r = slots + (int64_t)r * max_tokens;
-    const int32_t* pos_r = positions + (int64_t)r * max_tokens;
+    const int64_t* slots_r = PLACE ? nullptr : slots + (int64_t)r * max_tokens;
+    const int32_t* pos_r = PLACE ? nullptr : positions + (int64_t)r * max_tokens;
+    int64_t* out_slots_r = PLACE ? pl.out_slots + (int64_t)r * max_tokens : nullptr;
+    int32_t* out_pos_r = PLACE ? pl.out_positions + (int64_t)r * max_tokens : nullptr;
 
     const int64_t row_units = (int64_t)H * D / 8;  // 16-byte units per (token, layer) row
     const int half_units = D >> 4;                 // 16-byte units in half a head
@@ -216,8 +296,24 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
                 if (s_b[mid] <= token) lo = mid; else hi = mid - 1;
             }
             const int64_t off = s_off[lo];
-            const int64_t slot = slots_r[token];
-            const int32_t pos = pos_r[token];
+            int64_t slot;
+            int32_t pos;
+            if (PLACE) {
+                // position start_pos + idx, slot through the block table
+                // (start_pos + max_tokens < 2^31, checked on the host); the
+                // first lane unit of each token, in the first layer group,
+                // writes the token's slot and position out
+                pos = pl.start_pos + token;
+                const int32_t blk = pos / pl.page_size;
+                slot = (int64_t)bt_r[blk] * pl.page_size + (pos - blk * pl.page_size);
+                if (lg == 0 && lu == 0) {
+                    out_slots_r[token] = slot;
+                    out_pos_r[token] = pos;
+                }
+            } else {
+                slot = slots_r[token];
+                pos = pos_r[token];
+            }
             if (off >= 0) {
                 const int64_t src = off + (token - s_b[lo]);
                 const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
@@ -288,12 +384,15 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          int32_t k, int32_t nq, int64_t n, int64_t lens_stride,
                          int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
                          int64_t T_store, int64_t num_slots, const double* inv_freq,
-                         int32_t interleaved, uint32_t* status, hipStream_t st) {
+                         int32_t interleaved, uint32_t* status, hipStream_t st,
+                         const PlaceArgs* place) {
     if (k > kInjThreads) return hipErrorInvalidValue;
     const int64_t U = (int64_t)H * (D >> 4);
     const int64_t groups_max = ((int64_t)max_tokens * U + kWave - 1) / kWave;
     const int64_t items_max = groups_max * ((L + kInjLayers - 1) / kInjLayers);
-    if (items_max == 0) return hipSuccess;
+    // with nothing to place the plain inject has no work; the fused launch
+    // still runs to validate the requests and write m
+    if (items_max == 0 && !place) return hipSuccess;
     // one workgroup per CU, shared by the requests; the shape depends on
     // max_tokens only, never on m
     const int cus = compute_units();
@@ -307,28 +406,32 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 &&
         !lds_attr_set[dev].load(std::memory_order_acquire)) {
-        hipError_t e = hipFuncSetAttribute((const void*)inject_kernel<false>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)kInjLdsReserve);
-        if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void*)inject_kernel<true>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    (int)kInjLdsReserve);
-        if (e != hipSuccess) return e;
+        const void* fns[4] = {(const void*)inject_kernel<false, false>,
+                              (const void*)inject_kernel<true, false>,
+                              (const void*)inject_kernel<false, true>,
+                              (const void*)inject_kernel<true, true>};
+        for (const void* fn : fns) {
+            const hipError_t e = hipFuncSetAttribute(
+                fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kInjLdsReserve);
+            if (e != hipSuccess) return e;
+        }
         lds_attr_set[dev].store(true, std::memory_order_release);
     }
-    if (interleaved)
-        hipLaunchKernelGGL(inject_kernel<true>, grid, dim3(kInjThreads), kInjLdsReserve, st, ids,
-                           (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
-                           (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
-                           lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
-                           inv_freq, status);
-    else
-        hipLaunchKernelGGL(inject_kernel<false>, grid, dim3(kInjThreads), kInjLdsReserve, st, ids,
-                           (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,
-                           (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,
-                           lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
-                           inv_freq, status);
+    const PlaceArgs pl = place ? *place : PlaceArgs{};
+#define IS_LAUNCH_INJECT(IL, PLACE)                                                                \
+    hipLaunchKernelGGL((inject_kernel<IL, PLACE>), grid, dim3(kInjThreads), kInjLdsReserve, st,   \
+                       ids, (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,     \
+                       (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,         \
+                       lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,         \
+                       inv_freq, status, pl)
+    if (place) {
+        if (interleaved) IS_LAUNCH_INJECT(true, true);
+        else IS_LAUNCH_INJECT(false, true);
+    } else {
+        if (interleaved) IS_LAUNCH_INJECT(true, false);
+        else IS_LAUNCH_INJECT(false, false);
+    }
+#undef IS_LAUNCH_INJECT
     return hipGetLastError();
 }
 

@@ -51,13 +51,24 @@ hipError_t launch_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t
                            int32_t reverse_rank, uint32_t* status, hipStream_t st);
 
 // inject.hip
+// Placement inputs and outputs of the fused place + inject launch.
+struct PlaceArgs {
+    const int32_t* block_table;  // [nq][max_blocks]
+    int64_t* out_slots;          // [nq][max_tokens]
+    int32_t* out_positions;      // [nq][max_tokens]
+    int32_t* out_m;              // [nq]
+    int32_t start_pos, page_size, max_blocks;
+};
+// place == nullptr: slots, positions and m are the slot map's outputs.
+// Otherwise they are ignored and the launch places the facts itself.
 hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
                          const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,
                          const int64_t* fact_offsets, const int32_t* fact_lens, const int32_t* m,
                          int32_t k, int32_t nq, int64_t n, int64_t lens_stride,
                          int32_t reverse_rank, int32_t max_tokens, int32_t L, int32_t H, int32_t D,
                          int64_t T_store, int64_t num_slots, const double* inv_freq,
-                         int32_t interleaved, uint32_t* status, hipStream_t st);
+                         int32_t interleaved, uint32_t* status, hipStream_t st,
+                         const PlaceArgs* place = nullptr);
 
 // consumer.hip
 int consumer_max_q_elems();

@@ -7,7 +7,8 @@ import torch
 
 from . import (IS_DTYPE_BF16, IS_DTYPE_F32, IS_ROPE_HALF_SPLIT, is_ann_build,
                is_ann_build_workspace_size, is_ann_search, is_ann_search_workspace_size,
-               is_inject, is_inject_rotary, is_retrieve, is_retrieve_workspace_size, is_slot_map)
+               is_inject, is_inject_rotary, is_place_inject, is_retrieve,
+               is_retrieve_workspace_size, is_slot_map)
 
 
 class RequestBuffers:
@@ -62,10 +63,25 @@ class RequestBuffers:
                              paged_v, inv_freq=inv_freq, pairing=pairing, **kw)
 
 
+    def place_inject(self, preK, V, rope_theta, paged_k, paged_v, *, fact_offsets, fact_lens,
+                     lens_stride, start_pos, block_table, page_size, reverse_rank=1,
+                     inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, stream=None):
+        L, T_store, H, D = preK.shape
+        is_place_inject(self.ids, preK, V, rope_theta, paged_k, paged_v, self.slots,
+                        self.positions, self.m, fact_offsets=fact_offsets, fact_lens=fact_lens,
+                        start_pos=start_pos, block_table=block_table, page_size=page_size,
+                        max_blocks=block_table.shape[-1], k=self.k, nq=self.nq, n=self.n,
+                        lens_stride=lens_stride, reverse_rank=reverse_rank,
+                        max_tokens=self.max_tokens, L=L, H=H, D=D, T_store=T_store,
+                        num_slots=paged_k.shape[1], inv_freq=inv_freq, pairing=pairing,
+                        status=self.status, stream=stream)
+
+
 def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, paged_v, *,
                 start_pos, page_size, rope_theta, shared_bank=True, reverse_rank=1,
-                inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, stream=None):
-    """Enqueue retrieve -> slot map -> inject for every request of ``buf``.
+                inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, fused=False, stream=None):
+    """Enqueue retrieve -> slot map -> inject for every request of ``buf``
+    (``fused``: retrieve -> one place + inject launch, same results).
 
     ``store`` is a dict with preK, V ([L][T_store][H][D] bf16), fact_lens
     ([banks][n] int32) and fact_offsets ([banks][n] int64)."""
@@ -73,6 +89,13 @@ def run_request(buf: RequestBuffers, query, bank, store, block_table, paged_k, p
     bank_stride = 0 if shared_bank else n * d
     lens_stride = 0 if store["fact_lens"].shape[0] == 1 else n
     buf.retrieve(query, bank, bank_stride=bank_stride, stream=stream)
+    if fused:
+        buf.place_inject(store["preK"], store["V"], rope_theta, paged_k, paged_v,
+                         fact_offsets=store["fact_offsets"], fact_lens=store["fact_lens"],
+                         lens_stride=lens_stride, start_pos=start_pos, block_table=block_table,
+                         page_size=page_size, reverse_rank=reverse_rank, inv_freq=inv_freq,
+                         pairing=pairing, stream=stream)
+        return
     buf.slot_map(store["fact_lens"], start_pos, block_table, page_size, lens_stride=lens_stride,
                  reverse_rank=reverse_rank, stream=stream)
     buf.inject(store["preK"], store["V"], rope_theta, paged_k, paged_v,

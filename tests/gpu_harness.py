@@ -44,11 +44,13 @@ class Instance:
         self.buf = RequestBuffers(n=w.n, d=w.d_e, k=w.k, nq=w.nq, emb_dtype=self.bank.dtype,
                                   max_tokens=self.max_tokens, device=device)
 
-    def run(self, reverse_rank=1, inv_freq=None, interleaved=False, stream=None, sync=True):
+    def run(self, reverse_rank=1, inv_freq=None, interleaved=False, stream=None, sync=True,
+            fused=False):
         """One pass; inv_freq (float64 numpy [D/2]) and interleaved select the
         rotary table and pair layout (kept for the checks). ``stream`` (a
-        torch stream, default the current one) takes the three calls; with
-        ``sync=False`` the pass is left in flight."""
+        torch stream, default the current one) takes the calls; with
+        ``sync=False`` the pass is left in flight; ``fused`` replaces the slot
+        map and inject calls by the one place + inject call."""
         from paper_2607_27090_amd import IS_ROPE_HALF_SPLIT, IS_ROPE_INTERLEAVED
         w = self.w
         self.inv_freq, self.interleaved = inv_freq, bool(interleaved)
@@ -58,7 +60,7 @@ class Instance:
                     start_pos=w.start_pos, page_size=w.page_size, rope_theta=w.theta,
                     shared_bank=w.shared_bank, reverse_rank=reverse_rank, inv_freq=tf,
                     pairing=IS_ROPE_INTERLEAVED if interleaved else IS_ROPE_HALF_SPLIT,
-                    stream=stream)
+                    fused=fused, stream=stream)
         if sync:
             torch.cuda.synchronize()
 

@@ -149,6 +149,43 @@ def test_inject_rotary_rejects(kw, code):
     assert _rotary(**kw) == code
 
 
+def _place_inject(**kw):
+    a = dict(ids=A, K=A, V=A, offs=A, lens=A, start=0, bt=A, P=16, mb=10, theta=500000.0,
+             f=None, pairing=0, pk=A, pv=A, slots=A, pos=A, m=A, k=5, nq=1, n=100, ls=0, rev=1,
+             mt=100, L=2, H=8, D=128, T=1000, ns=1000, status=A)
+    a.update(kw)
+    return isl.load_library().is_place_inject(
+        a["ids"], a["K"], a["V"], a["offs"], a["lens"], a["start"], a["bt"], a["P"], a["mb"],
+        a["theta"], a["f"], a["pairing"], a["pk"], a["pv"], a["slots"], a["pos"], a["m"], a["k"],
+        a["nq"], a["n"], a["ls"], a["rev"], a["mt"], a["L"], a["H"], a["D"], a["T"], a["ns"],
+        a["status"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(ids=None), isl.IS_ERR_INVALID), (dict(K=None), isl.IS_ERR_INVALID),
+    (dict(bt=None), isl.IS_ERR_INVALID), (dict(slots=None), isl.IS_ERR_INVALID),
+    (dict(pos=None), isl.IS_ERR_INVALID), (dict(m=None), isl.IS_ERR_INVALID),
+    (dict(pk=None), isl.IS_ERR_INVALID), (dict(k=0), isl.IS_ERR_INVALID),
+    (dict(k=1025), isl.IS_ERR_INVALID), (dict(nq=0), isl.IS_ERR_INVALID),
+    (dict(nq=70000), isl.IS_ERR_INVALID), (dict(n=0), isl.IS_ERR_INVALID),
+    (dict(P=0), isl.IS_ERR_INVALID), (dict(start=-1), isl.IS_ERR_INVALID),
+    (dict(mb=-1), isl.IS_ERR_INVALID), (dict(mt=-1), isl.IS_ERR_INVALID),
+    (dict(start=2 ** 31 - 10), isl.IS_ERR_INVALID), (dict(ls=-1), isl.IS_ERR_INVALID),
+    (dict(L=0), isl.IS_ERR_INVALID), (dict(D=24), isl.IS_ERR_UNSUPPORTED),
+    (dict(D=528), isl.IS_ERR_UNSUPPORTED), (dict(T=-1), isl.IS_ERR_INVALID),
+    (dict(ns=-1), isl.IS_ERR_INVALID), (dict(theta=0.0), isl.IS_ERR_INVALID),
+    (dict(theta=float("nan")), isl.IS_ERR_INVALID), (dict(pairing=2), isl.IS_ERR_INVALID),
+    (dict(f=A + 4), isl.IS_ERR_INVALID), (dict(K=A + 8), isl.IS_ERR_INVALID),
+    (dict(slots=A + 4), isl.IS_ERR_INVALID), (dict(bt=A + 2), isl.IS_ERR_INVALID),
+    (dict(m=A + 2), isl.IS_ERR_INVALID), (dict(status=A + 1), isl.IS_ERR_INVALID),
+    # every argument valid: the pointer check refuses a fake store
+    (dict(), isl.IS_ERR_INVALID),
+])
+def test_place_inject_rejects(kw, code):
+    assert _place_inject(**kw) == code
+    assert isl.load_library().is_last_error().decode()
+
+
 def _scores(**kw):
     a = dict(q=A, qpos=A, pk=A, layer=0, bt=A, P=16, start=0, m=A, sc=A, nq=1, Hq=32, H=8,
              D=128, L=2, ns=1000, mb=10, mt=100, theta=500000.0, f=None, pairing=0, status=A)

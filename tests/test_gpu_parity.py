@@ -44,6 +44,20 @@ def test_llama8b_full_chain(llama_store, k):
     log(f"llama8b k={k}: m={int(o['m'][0])}, near-tie swaps {near}, floor-rescued {floor}")
 
 
+@pytest.mark.parametrize("k", [5, 50])
+def test_llama8b_fused_place_inject(llama_store, k):
+    # retrieval, then placement and injection in one launch
+    store, bank = llama_store
+    w = workloads.LLAMA8B.with_(k=k)
+    inst = Instance(w, store=store, bank=bank, variant=100 + k)
+    inst.buf.m.fill_(-7)
+    inst.run(fused=True)
+    near = inst.check_retrieve()
+    o = inst.check_slot_map()
+    floor = inst.check_inject_full()
+    log(f"llama8b fused k={k}: m={int(o['m'][0])}, near-tie swaps {near}, floor-rescued {floor}")
+
+
 def test_llama8b_deterministic(llama_store):
     store, bank = llama_store
     w = workloads.LLAMA8B
