@@ -24,7 +24,10 @@ def _pages(w, nb):
     return workloads.make_pages(w, nb, "cuda")[:2]
 
 
-def test_request_graph_replays_match_eager():
+@pytest.mark.parametrize("fused", [False, True])
+def test_request_graph_replays_match_eager(fused):
+    # fused: the graph holds retrieve + one place + inject launch, compared
+    # with the eager three-call path
     w = workloads.LLAMA8B.with_(n=3000, k=20, L=4, index=51)
     bank, store, bt, nb = _setup(w)
     q_in = workloads.make_queries(w, "cuda", variant=0).clone()
@@ -35,12 +38,12 @@ def test_request_graph_replays_match_eager():
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):  # warm-up on the capture stream
-        run_request(gbuf, q_in, bank, store, bt, gpk, gpv, **kw)
+        run_request(gbuf, q_in, bank, store, bt, gpk, gpv, fused=fused, **kw)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        run_request(gbuf, q_in, bank, store, bt, gpk, gpv, **kw)
+        run_request(gbuf, q_in, bank, store, bt, gpk, gpv, fused=fused, **kw)
     torch.cuda.synchronize()
     for v in (1, 2, 3, 1):
         q = workloads.make_queries(w, "cuda", variant=v)
@@ -61,7 +64,7 @@ def test_request_graph_replays_match_eager():
         assert torch.equal(gbuf.positions[:, :m], ebuf.positions[:, :m])
         assert torch.equal(gpk.view(torch.int16), epk.view(torch.int16)), v
         assert torch.equal(gpv.view(torch.int16), epv.view(torch.int16)), v
-        log(f"graph replay, query variant {v}: m={m}, equal to eager")
+        log(f"graph replay (fused={fused}), query variant {v}: m={m}, equal to eager")
 
 
 def test_filtered_retrieval_graph_replays_match_eager():
