@@ -19,7 +19,8 @@
 //     round robin to its workgroups, so all CUs sweep the request together
 //     (HBM serves one front of neighbouring addresses better than one
 //     contiguous share per CU: a plain copy of 526 MB runs at 5.6 TB/s in
-//     grid-stride order and at 4.5 TB/s with a contiguous share per CU);
+//     grid-stride order and at 4.5 TB/s with a contiguous share per CU), in
+//     an XCD-aware order: neighbouring items go to the workgroups of one XCD;
 //   * a workgroup is 16 waves and occupies a whole CU (the launch reserves
 //     more than half of the CU's LDS), and its waves take the workgroup's
 //     work items one at a time from a counter in LDS. The hardware issues the
@@ -256,11 +257,17 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     const int64_t ngroups = (items + kWave - 1) / kWave;      // 64-item groups
     const int64_t nlg = (L + kInjLayers - 1) / kInjLayers;     // layer groups
     const int64_t total = ngroups * nlg;
-    // this workgroup's items are blockIdx.x, blockIdx.x + G, ... (G = the
-    // request's workgroups), so at any moment all CUs work on neighbouring
-    // items: one front sweeping the request layer group by layer group
+    // this workgroup's items are base, base + G, ... (G = the request's
+    // workgroups), so at any moment all CUs work on neighbouring items: one
+    // front sweeping the request layer group by layer group. Workgroups are
+    // dealt to the 8 XCDs round robin (workgroup b of a request runs on XCD
+    // b % 8 when G is a multiple of 8), so base gives each XCD a run of G / 8
+    // consecutive items: the page and store rows of neighbouring tokens are
+    // then translated in one XCD's L2 TLB instead of in several
     const int64_t G = gridDim.x;
-    const int64_t span = (total - blockIdx.x + G - 1) / G;
+    const int64_t base =
+        G % 8 == 0 ? (int64_t)(blockIdx.x / 8) + (G / 8) * (blockIdx.x % 8) : blockIdx.x;
+    const int64_t span = (total - base + G - 1) / G;
     const int64_t* slots_r = PLACE ? nullptr : slots + (int64_t)r * max_tokens;
     const int32_t* pos_r = PLACE ? nullptr : positions + (int64_t)r * max_tokens;
     int64_t* out_slots_r = PLACE ? pl.out_slots + (int64_t)r * max_tokens : nullptr;
@@ -275,7 +282,7 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     if (lane == 0) j = atomicAdd(&s_next, 1);
     j = __shfl(j, 0, kWave);
     while ((int64_t)j < span) {
-        const int64_t wi = (int64_t)blockIdx.x + (int64_t)j * G;
+        const int64_t wi = base + (int64_t)j * G;
         // the wave's next item is taken now; the LDS round trip hides under
         // this item's loads
         int32_t jn = 0;
