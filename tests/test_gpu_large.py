@@ -1,14 +1,16 @@
 """GPU parity at the large workload shapes, sampled: every id (near-tie rule),
 score, slot, position and m of the sampled requests is checked against the
 oracle, plus ~1% of the injected (request, token, layer) rows, every fact's
-first and last token, and a sample of untouched page slots."""
+first and last token, and a sample of untouched page slots. Each shape runs
+both ways: placement and injection in one launch (the launch the bench
+times) and as the two separate calls."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads
-from paper_2607_27090_amd import is_inject, is_slot_map
+from paper_2607_27090_amd import is_inject, is_place_inject, is_slot_map
 from paper_2607_27090_amd.pipeline import RequestBuffers
 from tests import parity
 from tests.gpu_harness import Instance, host_emb, log
@@ -21,28 +23,33 @@ def _free():
     torch.cuda.empty_cache()
 
 
+def _both_paths(inst, name, frac):
+    for fused in (True, False):
+        if not fused:
+            workloads.fill_sentinel(inst.pk)
+            workloads.fill_sentinel(inst.pv)
+            inst.buf.m.fill_(-1)
+            inst.buf.slots.fill_(-1)
+            inst.buf.positions.fill_(-1)
+        inst.run(fused=fused)
+        near = inst.check_retrieve()
+        inst.check_slot_map()
+        rows, floor = inst.check_inject_sampled(frac=frac, seed=int(fused))
+        log(f"{name} ({'one launch' if fused else 'separate calls'}): m total "
+            f"{int(inst.buf.m.sum())}, near-tie swaps {near}, {rows} sampled rows, "
+            f"floor-rescued {floor}")
+
+
 def test_concurrency_64_users_per_user_banks():
-    w = workloads.CONCURRENCY
-    inst = Instance(w)
-    inst.run()
-    near = inst.check_retrieve()
-    inst.check_slot_map()
-    rows, floor = inst.check_inject_sampled(frac=0.01)
-    log(f"64 users: m total {int(inst.buf.m.sum())}, near-tie swaps {near}, "
-        f"{rows} sampled rows, floor-rescued {floor}")
+    inst = Instance(workloads.CONCURRENCY)
+    _both_paths(inst, "64 users", 0.01)
     del inst
     _free()
 
 
 def test_llama70b_shapes_8_queries():
-    w = workloads.LLAMA70B
-    inst = Instance(w)
-    inst.run()
-    near = inst.check_retrieve()
-    inst.check_slot_map()
-    rows, floor = inst.check_inject_sampled(frac=0.005)
-    log(f"70B shapes: m total {int(inst.buf.m.sum())}, near-tie swaps {near}, "
-        f"{rows} sampled rows, floor-rescued {floor}")
+    inst = Instance(workloads.LLAMA70B)
+    _both_paths(inst, "70B shapes", 0.005)
     del inst
     _free()
 
@@ -81,33 +88,44 @@ def test_retrieval_1m_bank_256_queries_injected_in_waves():
     bt, num_blocks = workloads.make_block_tables(ww, "cuda")
     pk, pv, num_slots = workloads.make_pages(ww, num_blocks, "cuda")
     lens = store["fact_lens"]
+    L, T, H, D = store["preK"].shape
     for w0 in range(0, w.nq, wave):
-        ids_w = buf.ids[w0:w0 + wave]
-        slots = buf.slots[w0:w0 + wave]
-        pos = buf.positions[w0:w0 + wave]
-        m = buf.m[w0:w0 + wave]
-        buf.status.zero_()
-        is_slot_map(ids_w, lens, w.start_pos, bt, w.page_size, slots, pos, m, k=w.k, nq=wave,
-                    n=w.n, lens_stride=0, max_blocks=bt.shape[1], max_tokens=w.max_tokens,
-                    status=buf.status)
-        L, T, H, D = store["preK"].shape
-        is_inject(ids_w, store["preK"], store["V"], slots, pos, w.theta, pk, pv,
-                  fact_offsets=store["fact_offsets"], fact_lens=lens, m=m, k=w.k, nq=wave, n=w.n,
-                  lens_stride=0, max_tokens=w.max_tokens, L=L, H=H, D=D, T_store=T,
-                  num_slots=num_slots, status=buf.status)
-        torch.cuda.synchronize()
-        assert int(buf.status.item()) == 0
-        # sampled check of this wave through the harness helpers
-        view = Instance.__new__(Instance)
-        view.w, view.store, view.bt = ww, store, bt
-        view.pk, view.pv, view.num_slots, view.max_tokens = pk, pv, num_slots, w.max_tokens
-        sub = RequestBuffers.__new__(RequestBuffers)
-        sub.ids, sub.slots, sub.positions, sub.m, sub.status = ids_w, slots, pos, m, buf.status
-        view.buf = sub
-        view.check_slot_map()
-        rows, floor = view.check_inject_sampled(frac=0.002, seed=w0)
-        log(f"1M bank wave {w0 // wave}: m total {int(m.sum())}, {rows} rows, floor {floor}")
-        workloads.fill_sentinel(pk)
-        workloads.fill_sentinel(pv)
+        for fused in (True, False):
+            ids_w = buf.ids[w0:w0 + wave]
+            slots = buf.slots[w0:w0 + wave]
+            pos = buf.positions[w0:w0 + wave]
+            m = buf.m[w0:w0 + wave]
+            m.fill_(-1)
+            buf.status.zero_()
+            if fused:
+                is_place_inject(ids_w, store["preK"], store["V"], w.theta, pk, pv, slots, pos, m,
+                                fact_offsets=store["fact_offsets"], fact_lens=lens,
+                                start_pos=w.start_pos, block_table=bt, page_size=w.page_size,
+                                max_blocks=bt.shape[1], k=w.k, nq=wave, n=w.n, lens_stride=0,
+                                max_tokens=w.max_tokens, L=L, H=H, D=D, T_store=T,
+                                num_slots=num_slots, status=buf.status)
+            else:
+                is_slot_map(ids_w, lens, w.start_pos, bt, w.page_size, slots, pos, m, k=w.k,
+                            nq=wave, n=w.n, lens_stride=0, max_blocks=bt.shape[1],
+                            max_tokens=w.max_tokens, status=buf.status)
+                is_inject(ids_w, store["preK"], store["V"], slots, pos, w.theta, pk, pv,
+                          fact_offsets=store["fact_offsets"], fact_lens=lens, m=m, k=w.k,
+                          nq=wave, n=w.n, lens_stride=0, max_tokens=w.max_tokens, L=L, H=H,
+                          D=D, T_store=T, num_slots=num_slots, status=buf.status)
+            torch.cuda.synchronize()
+            assert int(buf.status.item()) == 0
+            # sampled check of this wave through the harness helpers
+            view = Instance.__new__(Instance)
+            view.w, view.store, view.bt = ww, store, bt
+            view.pk, view.pv, view.num_slots, view.max_tokens = pk, pv, num_slots, w.max_tokens
+            sub = RequestBuffers.__new__(RequestBuffers)
+            sub.ids, sub.slots, sub.positions, sub.m, sub.status = ids_w, slots, pos, m, buf.status
+            view.buf = sub
+            view.check_slot_map()
+            rows, floor = view.check_inject_sampled(frac=0.002, seed=w0 + int(fused))
+            log(f"1M bank wave {w0 // wave} ({'one launch' if fused else 'separate calls'}): "
+                f"m total {int(m.sum())}, {rows} rows, floor {floor}")
+            workloads.fill_sentinel(pk)
+            workloads.fill_sentinel(pv)
     del store, pk, pv, bank
     _free()
