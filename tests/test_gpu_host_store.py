@@ -30,8 +30,15 @@ def test_inject_from_pinned_host_store_matches_oracle_and_device_store():
     assert torch.equal(a.buf.ids, b.buf.ids) and torch.equal(a.buf.slots, b.buf.slots)
     assert torch.equal(a.pk.view(torch.int16), b.pk.view(torch.int16))
     assert torch.equal(a.pv.view(torch.int16), b.pv.view(torch.int16))
-    log(f"host store: m={int(a.buf.m.sum())} tokens, pages equal to the device-store run, "
-        f"floor-rescued {floor}")
+    # the one-launch placement + inject reading the same host store
+    c = Instance(W, store=host, bank=a.bank)
+    c.run(fused=True)
+    assert torch.equal(a.buf.m, c.buf.m) and torch.equal(a.buf.slots, c.buf.slots)
+    assert torch.equal(a.buf.positions, c.buf.positions)
+    assert torch.equal(a.pk.view(torch.int16), c.pk.view(torch.int16))
+    assert torch.equal(a.pv.view(torch.int16), c.pv.view(torch.int16))
+    log(f"host store: m={int(a.buf.m.sum())} tokens, pages equal to the device-store run "
+        f"and to the one-launch path, floor-rescued {floor}")
 
 
 def test_pageable_host_store_is_rejected_before_launch():
@@ -49,6 +56,15 @@ def test_pageable_host_store_is_rejected_before_launch():
                        slots.data_ptr(), pos.data_ptr(), ctypes.c_float(W.theta), pk.data_ptr(),
                        pk.data_ptr(), dev["fact_offsets"].data_ptr(), dev["fact_lens"].data_ptr(),
                        m.data_ptr(), W.k, 1, W.n, 0, 1, 8, L, H, D, T, 64, None, None)
+    torch.cuda.synchronize()
+    assert rc == IS_ERR_INVALID
+    assert b"preK" in lib.is_last_error()
+    bt = torch.zeros(1, 8, dtype=torch.int32, device="cuda")
+    rc = lib.is_place_inject(ids.data_ptr(), pageable.ctypes.data, dev["V"].data_ptr(),
+                             dev["fact_offsets"].data_ptr(), dev["fact_lens"].data_ptr(), 0,
+                             bt.data_ptr(), 16, 8, ctypes.c_float(W.theta), None, 0,
+                             pk.data_ptr(), pk.data_ptr(), slots.data_ptr(), pos.data_ptr(),
+                             m.data_ptr(), W.k, 1, W.n, 0, 1, 8, L, H, D, T, 64, None, None)
     torch.cuda.synchronize()
     assert rc == IS_ERR_INVALID
     assert b"preK" in lib.is_last_error()
