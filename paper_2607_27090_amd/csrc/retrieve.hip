@@ -112,12 +112,8 @@ static hipError_t launch_scan_t(const void* query, const void* bank, int64_t n, 
                                 int64_t bank_stride_chunks, float* scores, hipStream_t st) {
     constexpr int RB = (CPL <= 2) ? 4 : (CPL <= 4 ? 2 : 1);
     const int groups = bank_stride_chunks ? nq : (nq + NQB - 1) / NQB;
-    // aim for >= ~2048 blocks in flight over the whole grid, but give every
-    // block at least 16 rows: a small bank (10,000 rows) is read once in a
-    // single round of loads, so its launch time is mostly dispatch, and 625
-    // blocks of 16 rows finish sooner than 1,250 of 8
+    // aim for >= ~2048 blocks in flight over the whole grid
     int64_t rpb = (n * groups + 2047) / 2048;
-    if (rpb < 16) rpb = 16;
     rpb = ((rpb + 4 * RB - 1) / (4 * RB)) * (4 * RB);
     if (rpb < 4 * RB) rpb = 4 * RB;
     if (rpb > 1024) rpb = 1024;

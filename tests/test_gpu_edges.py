@@ -36,6 +36,15 @@ def _ret_case(n, d, k, nq, dt, shared, seed):
     (777, 264, 7, 9, "bf16", True),          # ragged d, 9 queries over 2 groups
     (1000, 4096, 10, 2, "f32", True),        # long rows
     (3000, 8, 1, 4, "bf16", False),
+    # the single-chunk select's bound from offered wave maxima (k <= 96) and
+    # its radix fallback: too few rows to offer k maxima, k at the limit of
+    # the offered-maxima bound and one past it
+    (100, 32, 40, 1, "f32", True),
+    (64, 8, 63, 1, "f32", True),
+    (1000, 32, 96, 2, "f32", True),
+    (1000, 32, 97, 1, "f32", True),
+    (16384, 32, 96, 1, "f32", True),
+    (10000, 768, 50, 2, "f32", True),
     # matrix-core scan (shared bf16 bank, >= 32 queries): ragged rows, ragged
     # reduction chunks, partial query tiles and more queries than one tile
     (1000, 64, 10, 32, "bf16", True),
