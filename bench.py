@@ -486,6 +486,21 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 5 * 2 * (1 << 30) / (a.elapsed_time(b) * 1e-3) / 1e9
     del src, dst
+    # with the store in host memory: a plain pinned-host -> device copy of
+    # 1 GiB, the practical ceiling of the host link in this process
+    pcie_gbps = None
+    if host_store:
+        hsrc = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+        ddst = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        ddst.copy_(hsrc, non_blocking=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(3):
+            ddst.copy_(hsrc, non_blocking=True)
+        b.record()
+        torch.cuda.synchronize()
+        pcie_gbps = 3 * (1 << 30) / (a.elapsed_time(b) * 1e-3) / 1e9
+        del hsrc, ddst
 
     # ---- CPU baseline: the oracle on the host for a bounded sample ------------
     cpu = None
@@ -543,6 +558,7 @@ def main():
             "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
             "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
+        "pcie_copy_ceiling_GBps": None if pcie_gbps is None else round(pcie_gbps, 1),
         "consumer": consumer,
         "ann": ann,
         "roofline": {
