@@ -376,6 +376,25 @@ def main():
         latency_ms = timed(1) / args.steps
         log(f"one stream: {latency_ms * 1e3:.1f} us/step")
 
+    # ---- per-request latency spread: the same K steps back to back with one
+    # event at each step boundary (the steps still queue behind each other)
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    bounds[0].record()
+    for si, i in enumerate(range(args.warmup, nsteps)):
+        step(i)
+        bounds[si + 1].record()
+    torch.cuda.synchronize()
+    per_req = sorted(bounds[j].elapsed_time(bounds[j + 1]) * 1e3 / w.nq for j in range(args.steps))
+
+    def pct(p_):
+        return per_req[min(len(per_req) - 1, int(round(p_ * (len(per_req) - 1))))]
+
+    latency_pct = {"p10": round(pct(0.1), 2), "p50": round(pct(0.5), 2),
+                   "p90": round(pct(0.9), 2)}
+    log(f"per-request latency: p10 {latency_pct['p10']} p50 {latency_pct['p50']} "
+        f"p90 {latency_pct['p90']} us")
+
     # ---- cold caches: each step alone after 1 GiB of writes (untimed) -------
     # evicts the bank, the placement arrays and any page lines from the
     # 256 MB Infinity Cache and the L2s; events bracket the step only
@@ -550,6 +569,7 @@ def main():
         "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
                         if args.detail else None),
         "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
+        "us_per_request_percentiles": latency_pct,
         "cold_cache_us_per_step_median": None if cold_ms is None else round(cold_ms * 1e3, 2),
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
         "inject_GBps": round(achieved, 1),
@@ -586,6 +606,17 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def measured_traffic(fused):
@@ -632,7 +663,8 @@ def ann_cpu_baseline(w, bank, index, query, ann, args, torch):
         done += 1
     el = time.perf_counter() - t0
     log(f"cpu oracle (graph search): {done} queries, {el:.1f}s")
-    return {"value": round(el / done * 1e6, 1), "unit": "us/query", "cores": 1, "kind": "oracle",
+    return {"value": round(el / done * 1e6, 1), "unit": "us/query", "cores": 1,
+            "cpu_model": _cpu_model(), "kind": "oracle",
             "sample": f"{done} of the {w.nq} queries of one step, the same graph and seeds"}
 
 
@@ -689,6 +721,7 @@ def cpu_baseline(w, bank, store, queries, bts, args, torch):
         "value": round(us, 1),
         "unit": "us/request",
         "cores": 1,
+        "cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": (f"{done} whole requests (scores over all {w.n} facts, full sort, slot map, "
                    f"fp64 RoPE inject of all {tokens} placed tokens x {L} layers), single thread"),
