@@ -524,7 +524,8 @@ def main():
     # ---- CPU baseline: the oracle on the host for a bounded sample ------------
     cpu = None
     if not args.no_cpu_baseline and args.workload == "llama8b" and not host_store and ann is None:
-        cpu = cpu_baseline(w, bank, store, queries, bts, args, torch)
+        cpu = cpu_baseline(w, bank, store, queries, bts, args, torch,
+                           gpu={"sets": sets, "pk": pk, "pv": pv, "graph": args.graph})
 
     out = {
         "metric": "µs per request (retrieve+RoPE-inject) at k=50; inject HBM GB/s vs peak",
@@ -668,24 +669,37 @@ def ann_cpu_baseline(w, bank, index, query, ann, args, torch):
             "sample": f"{done} of the {w.nq} queries of one step, the same graph and seeds"}
 
 
-def cpu_baseline(w, bank, store, queries, bts, args, torch):
+def cpu_baseline(w, bank, store, queries, bts, args, torch, gpu=None):
     """Time the oracle (single thread) on whole requests of the same workload:
-    full-bank scores + full sort + slot map + inject of every token."""
+    full-bank scores + full sort + slot map + inject of every token. The
+    requests are taken from the last timed step backwards; for those whose
+    page region no later step rewrote, the oracle's results are compared with
+    what the GPU wrote (`gpu`: the per-step buffers and the page pools)."""
     import numpy as np
     import oracle
 
     def u16(t):
         return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
+    def bf16_f64(x):
+        return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+    def ordered(x):  # bf16 bit patterns as integers in value order
+        x = x.astype(np.int64)
+        return np.where(x & 0x8000, -(x & 0x7FFF), x & 0x7FFF)
+
     bank_h = bank.cpu().numpy()
     lens = store["fact_lens"].cpu().numpy()
     offs = store["fact_offsets"].cpu().numpy()
     L, T, H, D = store["preK"].shape
     R = bts.shape[0]
+    last = args.warmup + args.steps - 1
     done, spent, tokens = 0, 0.0, 0
-    first = args.warmup
-    while spent < args.cpu_seconds and first + done < args.warmup + args.steps:
-        i = first + done
+    par = {"requests": 0, "ids_equal": 0, "placement_equal": True, "v_bit_exact": True,
+           "k_in_tolerance": True, "k_elements": 0, "k_not_bit_exact": 0, "k_max_ulp": 0,
+           "k_floor_rescued": 0}
+    while spent < args.cpu_seconds and done < args.steps:
+        i = last - done
         q = queries[i].cpu().numpy()
         bt = bts[i % R].cpu().numpy()
         # untimed: pull the rows the oracle will read into host memory
@@ -713,10 +727,48 @@ def cpu_baseline(w, bank, store, queries, bts, args, torch):
         oracle.inject(ids, Kc, Vc, sm["slots"], sm["positions"], w.theta, hk, hv, coffs, lens,
                       sm["m"], w.k, 1, w.n, 0, 1, w.max_tokens, L, H, D, cur, num_slots)
         spent += time.perf_counter() - t0
-        tokens += int(sm["m"][0])
+        m = int(sm["m"][0])
+        tokens += m
         done += 1
+        # untimed: the GPU's results for this request, while its pages are
+        # still in place (the last R steps; region 0 is reused by --graph)
+        if (gpu is None or par["requests"] >= 4 or i <= last - R
+                or (gpu["graph"] and i % R == 0)):
+            continue
+        g = gpu["sets"][i - args.warmup]
+        par["requests"] += 1
+        if not np.array_equal(g.ids[0].cpu().numpy(), ids[0]):
+            continue  # a near-tie swap: the pages then hold other facts
+        par["ids_equal"] += 1
+        slots = sm["slots"][0, :m]
+        par["placement_equal"] &= bool(
+            int(g.m[0]) == m and np.array_equal(g.slots[0, :m].cpu().numpy(), slots)
+            and np.array_equal(g.positions[0, :m].cpu().numpy(), sm["positions"][0, :m]))
+        sl = torch.from_numpy(slots).to(gpu["pk"].device)
+        gk, gv = u16(gpu["pk"][:, sl]), u16(gpu["pv"][:, sl])
+        ok_, ov_ = hk[:, slots], hv[:, slots]
+        par["v_bit_exact"] &= bool(np.array_equal(gv, ov_))
+        src = coffs[0, sm["fact"][0, :m]] + sm["tok"][0, :m]
+        for layer in range(L):  # one layer at a time keeps the temporaries small
+            gk2, ok2 = gk[layer].reshape(-1, D), ok_[layer].reshape(-1, D)
+            if np.array_equal(gk2, ok2):
+                par["k_elements"] += int(gk2.size)
+                continue
+            x = bf16_f64(Kc[layer, src].reshape(-1, D))
+            pair = np.hypot(x[:, :D // 2], x[:, D // 2:])
+            pair = np.concatenate([pair, pair], axis=1)
+            ulp = np.abs(ordered(gk2) - ordered(ok2))
+            err = np.abs(bf16_f64(gk2) - bf16_f64(ok2))
+            rel_ok = err <= 2.0 ** -7 * np.abs(bf16_f64(ok2))
+            floor_ok = err <= 2.0 ** -20 * pair
+            par["k_in_tolerance"] &= bool(((ulp <= 1) | rel_ok | floor_ok).all())
+            par["k_elements"] += int(gk2.size)
+            par["k_not_bit_exact"] += int((gk2 != ok2).sum())
+            par["k_max_ulp"] = max(par["k_max_ulp"], int(ulp.max()))
+            par["k_floor_rescued"] += int(((ulp > 1) & ~rel_ok & floor_ok).sum())
     us = spent / done * 1e6
-    log(f"cpu oracle: {done} requests, {spent:.1f}s, {us:.0f} us/request")
+    log(f"cpu oracle: {done} requests, {spent:.1f}s, {us:.0f} us/request; parity of "
+        f"{par['requests']} timed requests: {par}")
     return {
         "value": round(us, 1),
         "unit": "us/request",
@@ -725,6 +777,7 @@ def cpu_baseline(w, bank, store, queries, bts, args, torch):
         "kind": "oracle",
         "sample": (f"{done} whole requests (scores over all {w.n} facts, full sort, slot map, "
                    f"fp64 RoPE inject of all {tokens} placed tokens x {L} layers), single thread"),
+        "parity": par if gpu is not None else None,
     }
 
 
