@@ -325,3 +325,28 @@ def test_inject_flags_skip_only_the_bad_items():
     torch.cuda.synchronize()
     assert int(b.status.item()) & IS_DEV_ID_RANGE
     assert (inst.pk.view(torch.int16) == workloads.SENTINEL_BITS).all()
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_largest_request_count_per_launch(fused):
+    # 65,535 requests in one launch (the largest the library accepts): every
+    # per-request offset into ids, slots, positions, m and the block tables
+    # is at its largest. Placement of every request is checked against the
+    # oracle, retrieval and pages of a sample of requests.
+    w = workloads.TINY.with_(n=64, d_e=8, k=1, nq=65535, L=1, H=1, D=16, page_size=4,
+                             start_pos=0, len_lo=1, len_hi=2, index=401)
+    inst = Instance(w)
+    inst.run(fused=fused)
+    assert int(inst.buf.status.item()) == 0
+    inst.check_slot_map()
+    gids = inst.buf.ids.cpu().numpy()
+    qh, odt = host_emb(inst.query)
+    bh, _ = host_emb(inst.bank)
+    rng = np.random.default_rng(401)
+    near = 0
+    for r in [0, 1, 32767, w.nq - 1] + list(rng.integers(0, w.nq, 60)):
+        ids_o, _, s_all = oracle.retrieve(qh[r:r + 1], bh, w.n, w.d_e, w.k, 1, 0, odt)
+        near += parity.check_ids(gids[r], ids_o[0], s_all[0], w.n)
+    rows, floor = inst.check_inject_sampled(frac=0.05)
+    log(f"65,535 requests ({'one launch' if fused else 'separate calls'}): m total "
+        f"{int(inst.buf.m.sum())}, {rows} sampled rows, near-tie swaps {near}, floor {floor}")
