@@ -48,7 +48,7 @@
 namespace is {
 
 constexpr int kInjThreads = 1024;  // 16 waves: one workgroup fills a CU
-constexpr int kInjLayers = 2;      // layers of one work item
+constexpr int kInjLayers = 1;      // layers of one work item (2 and 4 measured slower)
 // dynamic LDS requested beyond the kernel's own, so that no two workgroups
 // share a CU (160 KiB of LDS per CU)
 constexpr size_t kInjLdsReserve = 84 * 1024;
@@ -303,24 +303,13 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
                 if (s_b[mid] <= token) lo = mid; else hi = mid - 1;
             }
             const int64_t off = s_off[lo];
-            int64_t slot;
-            int32_t pos;
-            if (PLACE) {
-                // position start_pos + idx, slot through the block table
-                // (start_pos + max_tokens < 2^31, checked on the host); the
-                // first lane unit of each token, in the first layer group,
-                // writes the token's slot and position out
-                pos = pl.start_pos + token;
-                const int32_t blk = pos / pl.page_size;
-                slot = (int64_t)bt_r[blk] * pl.page_size + (pos - blk * pl.page_size);
-                if (lg == 0 && lu == 0) {
-                    out_slots_r[token] = slot;
-                    out_pos_r[token] = pos;
-                }
-            } else {
-                slot = slots_r[token];
-                pos = pos_r[token];
-            }
+            // PLACE: position start_pos + idx and slot through the block table
+            // (start_pos + max_tokens < 2^31, checked on the host); the first
+            // lane unit of each token, in the first layer group, writes the
+            // token's slot and position out. The slot is formed after the
+            // item's data loads are issued (in both branches), so waiting for
+            // the block-table entry never delays them.
+            const bool writes_out = PLACE && lg == 0 && lu == 0;
             if (off >= 0) {
                 const int64_t src = off + (token - s_b[lo]);
                 const int64_t col = (int64_t)h * (D >> 3) + sub;  // 16-byte unit within the row
@@ -336,6 +325,20 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
                     khi[q] = load_nt(ksrc + so + half_units);
                     vlo[q] = load_nt(vsrc + so);
                     vhi[q] = load_nt(vsrc + so + half_units);
+                }
+                int64_t slot;
+                int32_t pos;
+                if (PLACE) {
+                    pos = pl.start_pos + token;
+                    const int32_t blk = pos / pl.page_size;
+                    slot = (int64_t)bt_r[blk] * pl.page_size + (pos - blk * pl.page_size);
+                    if (writes_out) {
+                        out_slots_r[token] = slot;
+                        out_pos_r[token] = pos;
+                    }
+                } else {
+                    slot = slots_r[token];
+                    pos = pos_r[token];
                 }
                 // the item's angles, computed while its loads are in flight:
                 // p * w_j formed in fp64, reduced to [-pi, pi] with a
@@ -376,6 +379,13 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
                         }
                     }
                 }
+            } else if (writes_out) {
+                // a fact whose rows are outside the store still gets its
+                // tokens' slots and positions, as the slot map gives them
+                const int32_t pos = pl.start_pos + token;
+                const int32_t blk = pos / pl.page_size;
+                out_slots_r[token] = (int64_t)bt_r[blk] * pl.page_size + (pos - blk * pl.page_size);
+                out_pos_r[token] = pos;
             }
         }
         j = __shfl(jn, 0, kWave);
