@@ -189,7 +189,7 @@ int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
  *   D              head dimension: a multiple of 16, <= IS_MAX_HEAD_DIM
  * Tokens whose slot lies outside [0, num_slots) and facts whose rows fall
  * outside the store are skipped and flagged.
- * Launch footprint: max(1, CUs / nq) workgroups of 1024 threads per request,
+ * Launch footprint: max(1, CUs / nq) workgroups of 768 threads per request,
  * each reserving 84 KiB of LDS so that it has its CU to itself; kernels on
  * other streams can share those CUs only within the remaining LDS and
  * registers.

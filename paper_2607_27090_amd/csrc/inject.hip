@@ -21,7 +21,7 @@
 //     contiguous share per CU: a plain copy of 526 MB runs at 5.6 TB/s in
 //     grid-stride order and at 4.5 TB/s with a contiguous share per CU), in
 //     an XCD-aware order: neighbouring items go to the workgroups of one XCD;
-//   * a workgroup is 16 waves and occupies a whole CU (the launch reserves
+//   * a workgroup is 12 waves and occupies a whole CU (the launch reserves
 //     more than half of the CU's LDS), and its waves take the workgroup's
 //     work items one at a time from a counter in LDS. The hardware issues the
 //     memory instructions of older waves first, so waves of one CU progress
@@ -47,7 +47,11 @@
 
 namespace is {
 
-constexpr int kInjThreads = 1024;  // 16 waves: one workgroup fills a CU
+// 12 waves, three per SIMD: one workgroup fills a CU. More waves in flight
+// serve this scattered pattern worse (1,024 threads were 1.8% slower, 512
+// threads 10% slower than 768)
+constexpr int kInjThreads = 768;
+constexpr int kInjFacts = 2;       // consecutive facts of the placement per thread in set-up
 constexpr int kInjLayers = 1;      // layers of one work item (2 and 4 measured slower)
 // dynamic LDS requested beyond the kernel's own, so that no two workgroups
 // share a CU (160 KiB of LDS per CU)
@@ -131,12 +135,17 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
 
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int r = blockIdx.y;
-    // m and this thread's fact id (fact t of the placement order, k <= the
-    // block size) are independent loads; the fact's length and store row
-    // depend only on the id and are loaded together
+    // m and this thread's fact ids (facts kInjFacts * t + f of the placement
+    // order) are independent loads; a fact's length and store row depend
+    // only on its id and are loaded together
     const int32_t m_in = PLACE ? 0 : m_dev[r];
     const int32_t* rid = ids + (int64_t)r * k;
-    const int32_t cid = t < k ? (reverse_rank ? rid[k - 1 - t] : rid[t]) : 0;
+    int32_t cid[kInjFacts];
+#pragma unroll
+    for (int f = 0; f < kInjFacts; ++f) {
+        const int i = kInjFacts * t + f;
+        cid[f] = i < k ? (reverse_rank ? rid[k - 1 - i] : rid[i]) : 0;
+    }
     // PLACE: the block-table entries of the blocks the first placed tokens
     // can use are independent of everything else and load now too
     const int32_t* bt_r = PLACE ? pl.block_table + (int64_t)r * pl.max_blocks : nullptr;
@@ -158,23 +167,30 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
     const int64_t* offs = fact_offsets + (int64_t)r * lens_stride;
     uint32_t flags = 0;
-    int64_t len = 0;
-    if (t < k) {
-        int64_t off = -1;
-        if (cid < 0 || (int64_t)cid >= n) {
-            flags |= IS_DEV_ID_RANGE;
-        } else {
-            const int32_t l = lens[cid];
-            const int64_t o = offs[cid];
-            if (l < 0) {
-                flags |= IS_DEV_BAD_LEN;
+    int64_t flen[kInjFacts];
+    int64_t len = 0;  // this thread's facts together
+#pragma unroll
+    for (int f = 0; f < kInjFacts; ++f) {
+        const int i = kInjFacts * t + f;
+        flen[f] = 0;
+        if (i < k) {
+            int64_t off = -1;
+            if (cid[f] < 0 || (int64_t)cid[f] >= n) {
+                flags |= IS_DEV_ID_RANGE;
             } else {
-                len = l;
-                if (o < 0 || o + l > T_store) flags |= IS_DEV_SRC_RANGE;
-                else off = o;
+                const int32_t l = lens[cid[f]];
+                const int64_t o = offs[cid[f]];
+                if (l < 0) {
+                    flags |= IS_DEV_BAD_LEN;
+                } else {
+                    flen[f] = l;
+                    if (o < 0 || o + l > T_store) flags |= IS_DEV_SRC_RANGE;
+                    else off = o;
+                }
             }
+            s_off[i] = off;
         }
-        s_off[t] = off;
+        len += flen[f];
     }
     if (t == 0) {
         s_flags = 0; s_bad = 0; s_bad_block = 0; s_next = 0;
@@ -189,13 +205,21 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     if (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN)) s_bad = 1;
     int64_t excl = incl - len;
     for (int w = 0; w < wave; ++w) excl += s_wave_tot[w];
-    if (t < k) s_b[t] = excl;
+#pragma unroll
+    for (int f = 0; f < kInjFacts; ++f) {
+        const int i = kInjFacts * t + f;
+        if (i < k) s_b[i] = excl;
+        excl += flen[f];
+    }
     if (t == 0) {
         int64_t tot = 0;
         for (int w = 0; w < kInjThreads / kWave; ++w) tot += s_wave_tot[w];
         s_b[k] = tot;
     }
-    if (t < k && (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN))) atomicOr(&s_flags, flags);
+    // a request-level failure reports only the id / length flags (a store
+    // range flag of the thread's other fact is reported with the items)
+    if (flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN))
+        atomicOr(&s_flags, flags & (IS_DEV_ID_RANGE | IS_DEV_BAD_LEN));
     if (PLACE) {
         // negative entries among the preloaded blocks; whether the placement
         // reaches them is known once the total is
@@ -403,7 +427,7 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          int64_t T_store, int64_t num_slots, const double* inv_freq,
                          int32_t interleaved, uint32_t* status, hipStream_t st,
                          const PlaceArgs* place) {
-    if (k > kInjThreads) return hipErrorInvalidValue;
+    if (k > kInjFacts * kInjThreads) return hipErrorInvalidValue;
     const int64_t U = (int64_t)H * (D >> 4);
     const int64_t groups_max = ((int64_t)max_tokens * U + kWave - 1) / kWave;
     const int64_t items_max = groups_max * ((L + kInjLayers - 1) / kInjLayers);
