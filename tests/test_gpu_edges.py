@@ -220,8 +220,9 @@ def test_place_inject_shapes(H, D, L, P, start, lo, hi, k, rev):
 
 
 def test_place_inject_largest_k():
-    # k = IS_MAX_K facts: every thread of the inject workgroup owns one fact
-    # of the placement prefix; zero-length facts mixed in
+    # k = IS_MAX_K facts: the inject workgroup's set-up threads own two facts
+    # each of the placement prefix (the first 512 threads busy, the rest
+    # empty); zero-length facts mixed in
     w = workloads.TINY.with_(L=2, n=2000, k=1024, len_lo=0, len_hi=3, index=71)
     inst = Instance(w)
     inst.run()
