@@ -589,8 +589,8 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": (measured_traffic(fused) if args.workload == "llama8b" and w.k == 50
-                        and args.rope == "default" else None),
+            "traffic": (measured_traffic(args.workload, fused)
+                        if args.k is None and args.rope == "default" else None),
             "traffic_unit": "HBM bytes per launch (scaled FETCH_SIZE + WRITE_SIZE)",
             "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves),
         } if not host_store else {
@@ -620,18 +620,33 @@ def _cpu_model():
     return None
 
 
-def measured_traffic(fused):
+# committed counter summaries per (workload at its default k, fused path):
+# file and the key of its per-launch figure
+TRAFFIC_PROFILES = {
+    ("llama8b", True): ("place_inject_llama8b_k50_traffic.md", "traffic_bytes_per_launch"),
+    ("llama8b", False): ("inject_kernel_llama8b_k50_traffic.md", "traffic_bytes_per_launch"),
+    ("concurrency", True): ("inject_kernel_concurrency64_k50.md", "traffic_bytes_per_launch"),
+    ("concurrency", False): ("inject_kernel_concurrency64_k50.md",
+                             "traffic_bytes_per_launch_separate"),
+    ("llama70b", True): ("inject_kernel_llama70b_k100.md", "traffic_bytes_per_launch"),
+    ("llama70b", False): ("inject_kernel_llama70b_k100.md", "traffic_bytes_per_launch_separate"),
+}
+
+
+def measured_traffic(workload, fused):
     """HBM bytes per inject launch from the committed counter summary of the
-    path timed, or None when the kernel sources changed since the counters
-    were taken."""
+    workload and path timed, or None when there is none or the kernel sources
+    changed since the counters were taken."""
     import hashlib
     import re
-    name = "place_inject" if fused else "inject_kernel"
-    path = os.path.join(ROOT, "profiles", f"{name}_llama8b_k50_traffic.md")
+    if (workload, fused) not in TRAFFIC_PROFILES:
+        return None
+    fname, key = TRAFFIC_PROFILES[(workload, fused)]
+    path = os.path.join(ROOT, "profiles", fname)
     csrc = os.path.join(ROOT, "paper_2607_27090_amd", "csrc")
     try:
         text = open(path).read()
-        tb = int(re.search(r"^traffic_bytes_per_launch: (\d+)", text, re.M).group(1))
+        tb = int(re.search(rf"^{key}: (\d+)", text, re.M).group(1))
         want = dict(re.findall(r"(\S+\.h\w*) ([0-9a-f]{64})", text))
     except (OSError, AttributeError):
         return None
