@@ -630,6 +630,9 @@ TRAFFIC_PROFILES = {
                              "traffic_bytes_per_launch_separate"),
     ("llama70b", True): ("inject_kernel_llama70b_k100.md", "traffic_bytes_per_launch"),
     ("llama70b", False): ("inject_kernel_llama70b_k100.md", "traffic_bytes_per_launch_separate"),
+    ("retrieval1m", True): ("inject_kernel_retrieval1m_k100.md", "traffic_bytes_per_launch"),
+    ("retrieval1m", False): ("inject_kernel_retrieval1m_k100.md",
+                             "traffic_bytes_per_launch_separate"),
 }
 
 
