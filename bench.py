@@ -105,6 +105,7 @@ def main():
     w = {"llama8b": workloads.LLAMA8B, "tiny": workloads.TINY,
          "concurrency": workloads.CONCURRENCY, "llama70b": workloads.LLAMA70B,
          "retrieval1m": workloads.RETRIEVAL1M}[args.workload]
+    default_k = w.k
     if args.k is not None:
         w = w.with_(k=args.k)
     host_store = args.store == "host"
@@ -590,7 +591,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": (measured_traffic(args.workload, fused)
-                        if args.k is None and args.rope == "default" else None),
+                        if w.k == default_k and args.rope == "default" else None),
             "traffic_unit": "HBM bytes per launch (scaled FETCH_SIZE + WRITE_SIZE)",
             "algorithmic_bytes_per_launch": round(statistics.fmean(inj_bytes) / nwaves),
         } if not host_store else {
