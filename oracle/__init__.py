@@ -48,9 +48,10 @@ _lib = None
 
 def build() -> str:
     """Compile oracle.c and ann.c into liboracle.so with gcc (strict IEEE, no
-    fast-math)."""
+    fast-math; OpenMP for the loops over independent outputs)."""
     cmd = ["gcc", "-O2", "-fPIC", "-shared", "-fno-fast-math", "-ffp-contract=off",
-           "-std=c11", "-Wall", "-Wno-maybe-uninitialized", "-o", _LIB, *_SRCS, "-lm"]
+           "-fopenmp", "-std=c11", "-Wall", "-Wno-maybe-uninitialized", "-o", _LIB, *_SRCS,
+           "-lm"]
     subprocess.run(cmd, check=True)
     return _LIB
 
@@ -64,6 +65,10 @@ def _load():
     lib = ctypes.CDLL(_LIB)
     P = ctypes.c_void_p
     i32, i64, f64, u16 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_uint16
+    lib.oracle_set_threads.argtypes = [i32]
+    lib.oracle_set_threads.restype = None
+    lib.oracle_threads.argtypes = []
+    lib.oracle_threads.restype = i32
     lib.oracle_bf16_to_double.argtypes = [u16]
     lib.oracle_bf16_to_double.restype = f64
     lib.oracle_double_to_bf16.argtypes = [f64]
@@ -118,6 +123,40 @@ def _ptr(a: np.ndarray | None):
 
 def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ---- threads ------------------------------------------------------------------
+
+_threads_setting = 0  # 0: the OpenMP default (OMP_NUM_THREADS, else every core)
+
+
+def set_threads(n: int) -> None:
+    """Threads of the scores, top-k and inject loops (0: the OpenMP default).
+    Results do not depend on it: every output is computed by one thread."""
+    global _threads_setting
+    _threads_setting = max(0, int(n))
+    _load().oracle_set_threads(_threads_setting)
+
+
+def threads() -> int:
+    """Threads the next scores / top-k / inject call will use."""
+    return int(_load().oracle_threads())
+
+
+class using_threads:
+    """Context manager: run the oracle on ``n`` threads inside the block."""
+
+    def __init__(self, n: int):
+        self.n = int(n)
+
+    def __enter__(self):
+        self._old = _threads_setting
+        set_threads(self.n)
+        return self
+
+    def __exit__(self, *exc):
+        set_threads(self._old)
+        return False
 
 
 # ---- number formats -------------------------------------------------------

@@ -33,8 +33,16 @@
  * Parity pins: every function here is pinned by the "not gpu" tests against
  * closed forms, brute force or an independent formulation (see the test
  * files named test_oracle_*.py).
+ *
+ * Threads: the scores, the top-k and the injection run their independent
+ * outputs (one score, one query's ranking, one (token, layer) row) on an
+ * OpenMP team of oracle_set_threads() threads (default: the OpenMP default,
+ * i.e. OMP_NUM_THREADS or every core). Each output is still computed by one
+ * thread in the order written below, so the results do not depend on the
+ * thread count; one thread is the plain serial program.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -50,6 +58,14 @@
 #define ORACLE_BAD_BLOCK 16u /* a block-table entry < 0                        */
 #define ORACLE_SLOT_RANGE 32u /* a slot outside [0, num_slots)                 */
 #define ORACLE_SRC_RANGE 64u /* a fact's rows fall outside [0, T_store)        */
+
+/* ---- threads -------------------------------------------------------------- */
+
+static int g_threads = 0; /* 0: the OpenMP default */
+
+void oracle_set_threads(int32_t n) { g_threads = n > 0 ? n : 0; }
+
+int32_t oracle_threads(void) { return g_threads > 0 ? g_threads : omp_get_max_threads(); }
 
 /* ---- number formats ---------------------------------------------------- */
 
@@ -107,19 +123,35 @@ int oracle_scores(const void* query, const void* bank, int64_t n, int32_t d,
 {
     if (!query || !bank || !out || n < 0 || d < 1 || nq < 1) return -1;
     if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
-    for (int32_t r = 0; r < nq; ++r) {
-        int64_t bank_base = (int64_t)r * bank_stride;
+    /* the queries decoded once (exact) */
+    double* qd = (double*)malloc((size_t)nq * d * sizeof(double));
+    if (!qd) return -2;
+    for (int64_t i = 0; i < (int64_t)nq * d; ++i) qd[i] = load_elem(query, i, dtype);
+    int failed = 0;
+    /* one bank row per iteration, decoded (exactly) once for every query
+     * that reads it; each score is summed over t = 0, 1, ... in order */
+#pragma omp parallel num_threads(oracle_threads()) reduction(|:failed)
+    {
+        double* ed = (double*)malloc((size_t)d * sizeof(double));
+        if (!ed) failed = 1;
+#pragma omp for schedule(static)
         for (int64_t j = 0; j < n; ++j) {
-            double s = 0.0;
-            for (int32_t t = 0; t < d; ++t) {
-                double qv = load_elem(query, (int64_t)r * d + t, dtype);
-                double ev = load_elem(bank, bank_base + j * (int64_t)d + t, dtype);
-                s += qv * ev;
+            if (!ed) continue;
+            for (int32_t r = 0; r < nq; ++r) {
+                if (r == 0 || bank_stride != 0) {
+                    const int64_t base = (int64_t)r * bank_stride + j * (int64_t)d;
+                    for (int32_t t = 0; t < d; ++t) ed[t] = load_elem(bank, base + t, dtype);
+                }
+                const double* qr = qd + (int64_t)r * d;
+                double s = 0.0;
+                for (int32_t t = 0; t < d; ++t) s += qr[t] * ed[t];
+                out[(int64_t)r * n + j] = s;
             }
-            out[(int64_t)r * n + j] = s;
         }
+        free(ed);
     }
-    return 0;
+    free(qd);
+    return failed ? -2 : 0;
 }
 
 /* ---- step 2: exact top-k by full sort (§3.2) -----------------------------
@@ -141,21 +173,28 @@ int oracle_topk(const double* scores, int64_t n, int32_t k, int32_t nq,
                 int32_t* out_ids, double* out_scores)
 {
     if (!scores || !out_ids || k < 1 || k > n || nq < 1) return -1;
-    scored_t* all = (scored_t*)malloc((size_t)n * sizeof(scored_t));
-    if (!all) return -2;
-    for (int32_t r = 0; r < nq; ++r) {
-        for (int64_t j = 0; j < n; ++j) {
-            all[j].s = scores[(int64_t)r * n + j];
-            all[j].id = j;
+    int failed = 0;
+    /* one query's full sort per iteration */
+#pragma omp parallel num_threads(oracle_threads()) reduction(|:failed)
+    {
+        scored_t* all = (scored_t*)malloc((size_t)n * sizeof(scored_t));
+        if (!all) failed = 1;
+#pragma omp for schedule(dynamic, 1)
+        for (int32_t r = 0; r < nq; ++r) {
+            if (!all) continue;
+            for (int64_t j = 0; j < n; ++j) {
+                all[j].s = scores[(int64_t)r * n + j];
+                all[j].id = j;
+            }
+            qsort(all, (size_t)n, sizeof(scored_t), by_score_desc_id_asc);
+            for (int32_t i = 0; i < k; ++i) {
+                out_ids[(int64_t)r * k + i] = (int32_t)all[i].id;
+                if (out_scores) out_scores[(int64_t)r * k + i] = all[i].s;
+            }
         }
-        qsort(all, (size_t)n, sizeof(scored_t), by_score_desc_id_asc);
-        for (int32_t i = 0; i < k; ++i) {
-            out_ids[(int64_t)r * k + i] = (int32_t)all[i].id;
-            if (out_scores) out_scores[(int64_t)r * k + i] = all[i].s;
-        }
+        free(all);
     }
-    free(all);
-    return 0;
+    return failed ? -2 : 0;
 }
 
 /* ---- step 3: placement and slot map (§5.2 Position policy; §2.2) ----------
@@ -324,6 +363,15 @@ int oracle_inject_rotary(const int32_t* ids, const uint16_t* preK, const uint16_
         oracle_default_inv_freq(rope_theta, D, freq);
     uint32_t flags = 0;
     int64_t row = (int64_t)H * D;
+    /* 1. the placement walk, in order: which stored row (or none) and which
+     *    slot and position each placed token of each request takes */
+    int64_t cap = 0;
+    for (int32_t r = 0; r < nq; ++r) cap += m[r] < max_tokens ? (m[r] > 0 ? m[r] : 0) : max_tokens;
+    int64_t* w_src = (int64_t*)malloc((size_t)(cap > 0 ? cap : 1) * sizeof(int64_t));
+    int64_t* w_slot = (int64_t*)malloc((size_t)(cap > 0 ? cap : 1) * sizeof(int64_t));
+    int64_t* w_pos = (int64_t*)malloc((size_t)(cap > 0 ? cap : 1) * sizeof(int64_t));
+    if (!w_src || !w_slot || !w_pos) { free(w_src); free(w_slot); free(w_pos); return -2; }
+    int64_t nw = 0;
     for (int32_t r = 0; r < nq; ++r) {
         const int32_t* rid = ids + (int64_t)r * k;
         const int32_t* lens = fact_lens + (int64_t)r * lens_stride;
@@ -345,21 +393,30 @@ int oracle_inject_rotary(const int32_t* ids, const uint16_t* preK, const uint16_
                 int64_t p = positions[(int64_t)r * max_tokens + idx];
                 if (slot < 0 || slot >= num_slots) { flags |= ORACLE_SLOT_RANGE; continue; }
                 if (!src_ok) continue;
-                int64_t src = off + t;
-                for (int32_t l = 0; l < L; ++l) {
-                    const uint16_t* ks = preK + ((int64_t)l * T_store + src) * row;
-                    const uint16_t* vs = V + ((int64_t)l * T_store + src) * row;
-                    uint16_t* kd = paged_k + ((int64_t)l * num_slots + slot) * row;
-                    uint16_t* vd = paged_v + ((int64_t)l * num_slots + slot) * row;
-                    for (int32_t h = 0; h < H; ++h)
-                        oracle_rope_table_bf16(ks + (int64_t)h * D, p, freq, D, interleaved,
-                                               kd + (int64_t)h * D);
-                    memcpy(vd, vs, (size_t)row * sizeof(uint16_t));
-                }
+                w_src[nw] = off + t;
+                w_slot[nw] = slot;
+                w_pos[nw] = p;
+                ++nw;
             }
             b += len;
         }
     }
+    /* 2. the writes: each (layer, head) takes every placed token in the
+     *    walk's order, so a slot written twice ends as in a serial run */
+#pragma omp parallel for collapse(2) schedule(dynamic, 1) num_threads(oracle_threads())
+    for (int32_t l = 0; l < L; ++l) {
+        for (int32_t h = 0; h < H; ++h) {
+            for (int64_t e = 0; e < nw; ++e) {
+                const int64_t so = ((int64_t)l * T_store + w_src[e]) * row + (int64_t)h * D;
+                const int64_t dst = ((int64_t)l * num_slots + w_slot[e]) * row + (int64_t)h * D;
+                oracle_rope_table_bf16(preK + so, w_pos[e], freq, D, interleaved, paged_k + dst);
+                memcpy(paged_v + dst, V + so, (size_t)D * sizeof(uint16_t));
+            }
+        }
+    }
+    free(w_src);
+    free(w_slot);
+    free(w_pos);
     if (status) *status |= flags;
     return 0;
 }

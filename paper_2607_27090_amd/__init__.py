@@ -125,11 +125,9 @@ def _check(fn: str, rc: int) -> None:
 
 
 def _ptr(x):
-    """Device pointer of a tensor (None -> NULL; ints pass through)."""
+    """Device pointer of a contiguous device tensor (None -> NULL)."""
     if x is None:
         return None
-    if isinstance(x, int):
-        return x
     if not isinstance(x, torch.Tensor):
         raise TypeError(f"expected a torch tensor, got {type(x)}")
     if not x.is_cuda:
@@ -139,6 +137,65 @@ def _ptr(x):
     return x.data_ptr()
 
 
+_I32 = (torch.int32,)
+_I64 = (torch.int64,)
+_F32 = (torch.float32,)
+_BF16 = (torch.bfloat16,)
+_F64 = (torch.float64,)
+_FLAGS = (torch.int32, getattr(torch, "uint32", torch.int32))
+
+
+class _Ptr:
+    """A checked tensor argument; becomes its pointer when the call is made."""
+    __slots__ = ("x", "store")
+
+    def __init__(self, x, store):
+        self.x, self.store = x, store
+
+
+def _arg(x, name: str, dtypes, numel: int, *, optional: bool = False, store: bool = False):
+    """Checks one tensor argument against the C ABI's element type and the
+    element count the call's shape arguments imply, so that a wrong dtype or
+    a short buffer is refused on the host instead of being read or written
+    past its end on the device. Every argument of a call is checked before
+    any of them is turned into a pointer (see _call)."""
+    if x is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(x, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(x).__name__}")
+    if x.dtype not in dtypes:
+        raise ValueError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, got {x.dtype}")
+    if x.numel() < numel:
+        raise ValueError(f"{name} holds {x.numel()} elements; the call needs at least {numel}")
+    return _Ptr(x, store)
+
+
+class _Stream:
+    """The stream argument of a call, looked up when the call is made."""
+    __slots__ = ("s",)
+
+    def __init__(self, s):
+        self.s = s
+
+
+def _call(fn: str, *args) -> None:
+    """Calls the C entry point `fn` with checked tensor arguments turned into
+    device (or pinned-host store) pointers and the stream looked up, and
+    raises on an error code."""
+    raw = [(_store_ptr(a.x) if a.store else _ptr(a.x)) if isinstance(a, _Ptr) else a
+           for a in args]
+    raw = [_resolve_stream(a.s) if isinstance(a, _Stream) else a for a in raw]
+    _check(fn, getattr(load_library(), fn)(*raw))
+
+
+def _table(n: int, nq: int, stride: int) -> int:
+    """Entries a per-request table with `stride` elements between requests
+    spans (stride 0: one shared table of n entries)."""
+    return n if stride == 0 else (nq - 1) * stride + n
+
+
 # torch's current raw stream without building a Stream object (the public
 # torch.cuda.current_stream() costs ~2.6 us of host time per call)
 _current_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
@@ -146,6 +203,10 @@ _current_device = getattr(torch._C, "_cuda_getDevice", None)
 
 
 def _stream(stream):
+    return _Stream(stream)
+
+
+def _resolve_stream(stream):
     if stream is None:
         if _current_raw_stream is not None and _current_device is not None:
             return _current_raw_stream(_current_device())
@@ -183,30 +244,60 @@ def is_retrieve(query_emb, bank, n, d, k, out_ids, out_scores=None, *, nq=1, ban
         raise ValueError("is_retrieve needs a workspace tensor "
                          "(is_retrieve_workspace_size bytes of device memory)")
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check("is_retrieve", load_library().is_retrieve(
-        _ptr(query_emb), _ptr(bank), n, d, k, _ptr(out_ids), _ptr(out_scores), nq, bank_stride,
-        dt, _ptr(workspace), ws_bytes, _stream(stream)))
+    _call("is_retrieve",
+        _arg(query_emb, "query_emb", (query_emb.dtype,), nq * d),
+        _arg(bank, "bank", (query_emb.dtype,), _table(n * d, nq, bank_stride)), n, d, k,
+        _arg(out_ids, "out_ids", _I32, nq * k),
+        _arg(out_scores, "out_scores", _F32, nq * k, optional=True), nq, bank_stride,
+        dt, _Ptr(workspace, False), ws_bytes, _stream(stream))
 
 
 def is_slot_map(ids, fact_lens, start_pos, block_table, page_size, out_slots, out_positions,
                 out_m, *, k, nq, n, lens_stride, max_blocks, max_tokens, reverse_rank=1,
                 status=None, stream=None) -> None:
     """Placement + slot map (see include/inferscale.h)."""
-    _check("is_slot_map", load_library().is_slot_map(
-        _ptr(ids), _ptr(fact_lens), start_pos, _ptr(block_table), page_size, _ptr(out_slots),
-        _ptr(out_positions), _ptr(out_m), k, nq, n, lens_stride, max_blocks, max_tokens,
-        reverse_rank, _ptr(status), _stream(stream)))
+    _call("is_slot_map",
+        _arg(ids, "ids", _I32, nq * k), _arg(fact_lens, "fact_lens", _I32,
+                                             _table(n, nq, lens_stride)),
+        start_pos, _arg(block_table, "block_table", _I32, nq * max_blocks), page_size,
+        _arg(out_slots, "out_slots", _I64, nq * max_tokens),
+        _arg(out_positions, "out_positions", _I32, nq * max_tokens),
+        _arg(out_m, "out_m", _I32, nq), k, nq, n, lens_stride, max_blocks, max_tokens,
+        reverse_rank, _arg(status, "status", _FLAGS, 1, optional=True), _stream(stream))
 
 
 def is_inject(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *, fact_offsets,
               fact_lens, m, k, nq, n, lens_stride, reverse_rank=1, max_tokens, L, H, D,
               T_store, num_slots, status=None, stream=None) -> None:
     """Fused gather + RoPE + scatter (see include/inferscale.h)."""
-    _check("is_inject", load_library().is_inject(
-        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(slots), _ptr(positions), float(rope_theta),
-        _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens), _ptr(m), k, nq, n,
-        lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots, _ptr(status),
-        _stream(stream)))
+    a = _inject_args(ids, preK, V, slots, positions, paged_k, paged_v, fact_offsets, fact_lens,
+                     m, k, nq, n, lens_stride, max_tokens, L, H, D, T_store, num_slots)
+    _call("is_inject",
+        a["ids"], a["preK"], a["V"], a["slots"], a["positions"], float(rope_theta), a["paged_k"],
+        a["paged_v"], a["fact_offsets"], a["fact_lens"], a["m"], k, nq, n, lens_stride,
+        reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+        _arg(status, "status", _FLAGS, 1, optional=True), _stream(stream))
+
+
+def _inject_args(ids, preK, V, slots, positions, paged_k, paged_v, fact_offsets, fact_lens, m,
+                 k, nq, n, lens_stride, max_tokens, L, H, D, T_store, num_slots):
+    """Checked pointers of the arguments is_inject and its variants share
+    (for is_place_inject, slots, positions and m are its outputs)."""
+    store = L * T_store * H * D
+    pages = L * num_slots * H * D
+    table = _table(n, nq, lens_stride)
+    return {
+        "ids": _arg(ids, "ids", _I32, nq * k),
+        "preK": _arg(preK, "preK", _BF16, store, store=True),
+        "V": _arg(V, "V", _BF16, store, store=True),
+        "slots": _arg(slots, "slots", _I64, nq * max_tokens),
+        "positions": _arg(positions, "positions", _I32, nq * max_tokens),
+        "paged_k": _arg(paged_k, "paged_k", _BF16, pages),
+        "paged_v": _arg(paged_v, "paged_v", _BF16, pages),
+        "fact_offsets": _arg(fact_offsets, "fact_offsets", _I64, table),
+        "fact_lens": _arg(fact_lens, "fact_lens", _I32, table),
+        "m": _arg(m, "m", _I32, nq),
+    }
 
 
 def is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_v, *,
@@ -215,13 +306,14 @@ def is_inject_rotary(ids, preK, V, slots, positions, rope_theta, paged_k, paged_
                      pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
     """is_inject with the model's rotary table (float64 device tensor [D/2],
     None: rope_theta's default table) and pair layout (see include/inferscale.h)."""
-    if inv_freq is not None and inv_freq.dtype != torch.float64:
-        raise ValueError("inv_freq must be a float64 tensor")
-    _check("is_inject_rotary", load_library().is_inject_rotary(
-        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(slots), _ptr(positions),
-        float(rope_theta), _ptr(paged_k), _ptr(paged_v), _ptr(fact_offsets), _ptr(fact_lens),
-        _ptr(m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
-        _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
+    a = _inject_args(ids, preK, V, slots, positions, paged_k, paged_v, fact_offsets, fact_lens,
+                     m, k, nq, n, lens_stride, max_tokens, L, H, D, T_store, num_slots)
+    _call("is_inject_rotary",
+        a["ids"], a["preK"], a["V"], a["slots"], a["positions"], float(rope_theta), a["paged_k"],
+        a["paged_v"], a["fact_offsets"], a["fact_lens"], a["m"], k, nq, n, lens_stride,
+        reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+        _arg(inv_freq, "inv_freq", _F64, D // 2, optional=True), int(pairing),
+        _arg(status, "status", _FLAGS, 1, optional=True), _stream(stream))
 
 
 def is_place_inject(ids, preK, V, rope_theta, paged_k, paged_v, out_slots, out_positions, out_m,
@@ -229,14 +321,16 @@ def is_place_inject(ids, preK, V, rope_theta, paged_k, paged_v, out_slots, out_p
                     nq, n, lens_stride, reverse_rank=1, max_tokens, L, H, D, T_store, num_slots,
                     inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
     """Slot map + inject in one launch (see include/inferscale.h)."""
-    if inv_freq is not None and inv_freq.dtype != torch.float64:
-        raise ValueError("inv_freq must be a float64 tensor")
-    _check("is_place_inject", load_library().is_place_inject(
-        _ptr(ids), _store_ptr(preK), _store_ptr(V), _ptr(fact_offsets), _ptr(fact_lens),
-        start_pos, _ptr(block_table), page_size, max_blocks, float(rope_theta), _ptr(inv_freq),
-        int(pairing), _ptr(paged_k), _ptr(paged_v), _ptr(out_slots), _ptr(out_positions),
-        _ptr(out_m), k, nq, n, lens_stride, reverse_rank, max_tokens, L, H, D, T_store,
-        num_slots, _ptr(status), _stream(stream)))
+    a = _inject_args(ids, preK, V, out_slots, out_positions, paged_k, paged_v, fact_offsets,
+                     fact_lens, out_m, k, nq, n, lens_stride, max_tokens, L, H, D, T_store,
+                     num_slots)
+    _call("is_place_inject",
+        a["ids"], a["preK"], a["V"], a["fact_offsets"], a["fact_lens"], start_pos,
+        _arg(block_table, "block_table", _I32, nq * max_blocks), page_size, max_blocks,
+        float(rope_theta), _arg(inv_freq, "inv_freq", _F64, D // 2, optional=True),
+        int(pairing), a["paged_k"], a["paged_v"], a["slots"], a["positions"], a["m"], k, nq, n,
+        lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,
+        _arg(status, "status", _FLAGS, 1, optional=True), _stream(stream))
 
 
 def is_paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, m, scores, *,
@@ -244,12 +338,14 @@ def is_paged_scores(q, qpos, paged_k, layer, block_table, page_size, start_pos, 
                     inv_freq=None, pairing=IS_ROPE_HALF_SPLIT, status=None, stream=None) -> None:
     """Attention logits of each request's query against its injected keys
     read through the block table (see include/inferscale.h)."""
-    if inv_freq is not None and inv_freq.dtype != torch.float64:
-        raise ValueError("inv_freq must be a float64 tensor")
-    _check("is_paged_scores", load_library().is_paged_scores(
-        _ptr(q), _ptr(qpos), _ptr(paged_k), layer, _ptr(block_table), page_size, start_pos,
-        _ptr(m), _ptr(scores), nq, Hq, H, D, L, num_slots, max_blocks, max_tokens,
-        float(rope_theta), _ptr(inv_freq), int(pairing), _ptr(status), _stream(stream)))
+    _call("is_paged_scores",
+        _arg(q, "q", _BF16, nq * Hq * D), _arg(qpos, "qpos", _I32, nq),
+        _arg(paged_k, "paged_k", _BF16, L * num_slots * H * D), layer,
+        _arg(block_table, "block_table", _I32, nq * max_blocks), page_size, start_pos,
+        _arg(m, "m", _I32, nq), _arg(scores, "scores", _F32, nq * Hq * max_tokens), nq, Hq, H,
+        D, L, num_slots, max_blocks, max_tokens, float(rope_theta),
+        _arg(inv_freq, "inv_freq", _F64, D // 2, optional=True), int(pairing),
+        _arg(status, "status", _FLAGS, 1, optional=True), _stream(stream))
 
 
 
@@ -269,9 +365,12 @@ def is_ann_build(bank, n, d, degree, graph, *, n_seeds=0, fwd=None, seed_ids=Non
         raise ValueError("is_ann_build needs a workspace tensor "
                          "(is_ann_build_workspace_size bytes of device memory)")
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check("is_ann_build", load_library().is_ann_build(
-        _ptr(bank), n, d, degree, dt, n_seeds, _ptr(graph), _ptr(fwd), _ptr(seed_ids),
-        _ptr(seed_bank), _ptr(workspace), ws_bytes, _stream(stream)))
+    _call("is_ann_build",
+        _arg(bank, "bank", (bank.dtype,), n * d), n, d, degree, dt, n_seeds,
+        _arg(graph, "graph", _I32, n * degree), _arg(fwd, "fwd", _I32, n * degree, optional=True),
+        _arg(seed_ids, "seed_ids", _I32, n_seeds, optional=n_seeds == 0),
+        _arg(seed_bank, "seed_bank", (bank.dtype,), n_seeds * d, optional=n_seeds == 0),
+        _Ptr(workspace, False), ws_bytes, _stream(stream))
 
 
 def is_ann_search_workspace_size(n_seeds: int, d: int, beam: int, nq: int = 1,
@@ -292,8 +391,14 @@ def is_ann_search(query_emb, bank, n, d, graph, degree, seed_ids, seed_bank, out
         raise ValueError("is_ann_search needs a workspace tensor "
                          "(is_ann_search_workspace_size bytes of device memory)")
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check("is_ann_search", load_library().is_ann_search(
-        _ptr(query_emb), nq, _ptr(bank), n, d, dt, _ptr(graph), degree, _ptr(seed_ids),
-        _ptr(seed_bank), n_seeds, beam, width, k, max_iters, _ptr(out_ids), _ptr(out_scores),
-        _ptr(out_iters), _ptr(out_scored), _ptr(status), _ptr(workspace), ws_bytes,
-        _stream(stream)))
+    et = (query_emb.dtype,)
+    _call("is_ann_search",
+        _arg(query_emb, "query_emb", et, nq * d), nq, _arg(bank, "bank", et, n * d), n, d, dt,
+        _arg(graph, "graph", _I32, n * degree), degree, _arg(seed_ids, "seed_ids", _I32, n_seeds),
+        _arg(seed_bank, "seed_bank", et, n_seeds * d), n_seeds, beam, width, k, max_iters,
+        _arg(out_ids, "out_ids", _I32, nq * k),
+        _arg(out_scores, "out_scores", _F32, nq * k, optional=True),
+        _arg(out_iters, "out_iters", _I32, nq, optional=True),
+        _arg(out_scored, "out_scored", _I32, nq, optional=True),
+        _arg(status, "status", _FLAGS, 1, optional=True), _Ptr(workspace, False), ws_bytes,
+        _stream(stream))

@@ -188,12 +188,18 @@ def test_search_clustered_bank_matches_oracle_and_recalls():
                           64, k, 256, width=1, dtype=odt)
     g_ids = ids.cpu().numpy()
     S = oracle.scores(Q, X, w.n, w.d_e, w.nq, 0, odt)
+    g_sc = sc.cpu().numpy()
+    qd = oracle.bf16_to_f64(Q) if odt == oracle.BF16 else Q.astype(np.float64)
     same = 0
     for q in range(w.nq):
-        # valid: distinct, ordered, scores within fp32 accumulation of exact
+        # valid: distinct ids, best first, each score within fp32 accumulation
+        # of the returned fact's exact score (magnitude sum_t |q_t e_t| of
+        # that fact, from the decoded values)
         assert len(set(g_ids[q].tolist())) == k
-        parity.check_scores(sc.cpu().numpy()[q], S[q, g_ids[q]],
-                            np.abs(Q[q].astype(np.float64)).sum() * np.ones(k))
+        assert np.all(np.diff(g_sc[q]) <= 0), f"query {q}: scores not in rank order"
+        rows = oracle.bf16_to_f64(X[g_ids[q]]) if odt == oracle.BF16 else \
+            X[g_ids[q]].astype(np.float64)
+        parity.check_scores(g_sc[q], S[q, g_ids[q]], np.abs(rows * qd[q]).sum(axis=1))
         same += int(np.array_equal(g_ids[q], r["ids"][q]))
     assert same >= w.nq - 2  # the walks diverge only where fp32 reorders a near tie
     ex_ids, _ = oracle.topk(S, k)
