@@ -23,7 +23,9 @@
  * Conventions shared by every call
  *   - All data pointers are DEVICE pointers owned by the caller. The library
  *     allocates and frees nothing; retrieval scratch is the caller's
- *     workspace, sized by is_retrieve_workspace_size.
+ *     workspace, sized by is_retrieve_workspace_size (is_retrieve_noalloc
+ *     instead uses a fixed scratch array of the library's, for callers that
+ *     cannot allocate).
  *   - `stream` is a hipStream_t (NULL: the legacy default stream). Every call
  *     only enqueues work on it and returns; none synchronizes. The calls keep
  *     no state between invocations and may run concurrently on different
@@ -125,6 +127,33 @@ int is_retrieve_workspace_size(int64_t n, int32_t d, int32_t k, int32_t nq, int3
 int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
                 int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
                 int32_t dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Largest scratch is_retrieve_noalloc uses (16 MiB per GPU). */
+#define IS_RETRIEVE_NOALLOC_MAX_BYTES ((size_t)16 << 20)
+
+/*
+ * is_retrieve_noalloc -- is_retrieve for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): no workspace argument, and no allocation of any kind.
+ *
+ * Arguments, results and errors are those of is_retrieve (same kernels, same
+ * output bits for the same inputs). Its scratch is a fixed array of
+ * IS_RETRIEVE_NOALLOC_MAX_BYTES in the library's own device memory, one per
+ * GPU, held from the first call on that GPU until the process ends; the
+ * first call on a GPU looks up that array's device address (no allocation).
+ * Sizes whose scratch (is_retrieve_workspace_size) exceeds the array are
+ * refused with IS_ERR_WORKSPACE before anything is enqueued: for example
+ * nq * n * 4 bytes of scores must fit (1 query: n up to ~4M; 8 queries over
+ * 100,000 facts fit; the filtered matrix-core path for many queries over a
+ * large bf16 bank does not).
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap in time on one GPU (on different streams, or
+ * from different threads) race and give undefined results. Calls on one
+ * stream, one after another, are safe.
+ */
+int is_retrieve_noalloc(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                        int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
+                        int32_t dtype, void* stream);
 
 /*
  * is_slot_map -- placement and slot mapping (§5.2 Position policy; §2.2).

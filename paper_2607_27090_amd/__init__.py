@@ -35,6 +35,7 @@ IS_DEV_SRC_RANGE = 64
 
 IS_MAX_K = 1024
 IS_MAX_HEAD_DIM = 512
+IS_RETRIEVE_NOALLOC_MAX_BYTES = 16 << 20
 
 IS_ROPE_HALF_SPLIT = 0
 IS_ROPE_INTERLEAVED = 1
@@ -45,7 +46,7 @@ IS_ANN_MAX_WIDTH = 4
 IS_ANN_MAX_EXPAND = 256
 
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_slot_map", "is_inject", "is_inject_rotary", "is_place_inject", "is_paged_scores",
+            "is_retrieve_noalloc", "is_slot_map", "is_inject", "is_inject_rotary", "is_place_inject", "is_paged_scores",
             "is_ann_build_workspace_size", "is_ann_build", "is_ann_search_workspace_size",
             "is_ann_search")
 
@@ -78,6 +79,8 @@ def load_library() -> ctypes.CDLL:
     lib.is_retrieve_workspace_size.restype = ctypes.c_int
     lib.is_retrieve.argtypes = [P, P, i64, i32, i32, P, P, i32, i64, i32, P, sz, P]
     lib.is_retrieve.restype = ctypes.c_int
+    lib.is_retrieve_noalloc.argtypes = [P, P, i64, i32, i32, P, P, i32, i64, i32, P]
+    lib.is_retrieve_noalloc.restype = ctypes.c_int
     lib.is_slot_map.argtypes = [P, P, i32, P, i32, P, P, P, i32, i32, i64, i64, i32, i32, i32, P, P]
     lib.is_slot_map.restype = ctypes.c_int
     lib.is_inject.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32, i32,
@@ -250,6 +253,19 @@ def is_retrieve(query_emb, bank, n, d, k, out_ids, out_scores=None, *, nq=1, ban
         _arg(out_ids, "out_ids", _I32, nq * k),
         _arg(out_scores, "out_scores", _F32, nq * k, optional=True), nq, bank_stride,
         dt, _Ptr(workspace, False), ws_bytes, _stream(stream))
+
+
+def is_retrieve_noalloc(query_emb, bank, n, d, k, out_ids, out_scores=None, *, nq=1,
+                        bank_stride=0, stream=None) -> None:
+    """is_retrieve with the library's fixed scratch array instead of a
+    workspace, for callers that cannot allocate (see include/inferscale.h)."""
+    dt = _emb_dtype(query_emb)
+    _call("is_retrieve_noalloc",
+        _arg(query_emb, "query_emb", (query_emb.dtype,), nq * d),
+        _arg(bank, "bank", (query_emb.dtype,), _table(n * d, nq, bank_stride)), n, d, k,
+        _arg(out_ids, "out_ids", _I32, nq * k),
+        _arg(out_scores, "out_scores", _F32, nq * k, optional=True), nq, bank_stride,
+        dt, _stream(stream))
 
 
 def is_slot_map(ids, fact_lens, start_pos, block_table, page_size, out_slots, out_positions,

@@ -258,6 +258,53 @@ int check_retrieve_sizes(int64_t n, int32_t d, int32_t k, int32_t nq, int32_t dt
     return IS_OK;
 }
 
+int check_retrieve_args(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                        const int32_t* out_ids, const float* out_scores, int32_t nq,
+                        int64_t bank_stride, int32_t dtype) {
+    if (!query_emb || !bank || !out_ids)
+        return fail(IS_ERR_INVALID, "query_emb, bank and out_ids must be non-NULL");
+    const int rc = check_retrieve_sizes(n, d, k, nq, dtype);
+    if (rc) return rc;
+    if (bank_stride < 0 || bank_stride % 8)
+        return fail(IS_ERR_INVALID, "bank_stride=%lld must be >= 0 and a multiple of 8",
+                    (long long)bank_stride);
+    if (!aligned(query_emb, 16) || !aligned(bank, 16))
+        return fail(IS_ERR_INVALID, "query_emb and bank must be 16-byte aligned");
+    if (!aligned(out_ids, 4) || (out_scores && !aligned(out_scores, 4)))
+        return fail(IS_ERR_INVALID, "out_ids/out_scores must be 4-byte aligned");
+    return IS_OK;
+}
+
+// Scratch of is_retrieve_noalloc: one array per GPU, in the library's own
+// device memory for as long as the process runs, so that the call allocates
+// nothing. Host code never uses the array's name as an address (on the host
+// it is only a stand-in for the symbol); it uses the device address that
+// hipGetSymbolAddress returns, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = IS_RETRIEVE_NOALLOC_MAX_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+// Device address of `scratch` on the current device (nullptr and *err set
+// on failure). Racing first calls on one device store the same address.
+void* noalloc_scratch(hipError_t* err) {
+    static std::atomic<void*> addr[64];
+    *err = hipSuccess;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= 64) {
+        *err = e != hipSuccess ? e : hipErrorInvalidDevice;
+        return nullptr;
+    }
+    void* p = addr[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+        *err = e != hipSuccess ? e : hipErrorInvalidSymbol;
+        return nullptr;
+    }
+    addr[dev].store(p, std::memory_order_release);
+    return p;
+}
+
 }  // namespace
 
 namespace is {
@@ -301,17 +348,9 @@ int is_retrieve_workspace_size(int64_t n, int32_t d, int32_t k, int32_t nq, int3
 int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
                 int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
                 int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
-    if (!query_emb || !bank || !out_ids)
-        return fail(IS_ERR_INVALID, "query_emb, bank and out_ids must be non-NULL");
-    int rc = check_retrieve_sizes(n, d, k, nq, dtype);
+    const int rc = check_retrieve_args(query_emb, bank, n, d, k, out_ids, out_scores, nq,
+                                       bank_stride, dtype);
     if (rc) return rc;
-    if (bank_stride < 0 || bank_stride % 8)
-        return fail(IS_ERR_INVALID, "bank_stride=%lld must be >= 0 and a multiple of 8",
-                    (long long)bank_stride);
-    if (!aligned(query_emb, 16) || !aligned(bank, 16))
-        return fail(IS_ERR_INVALID, "query_emb and bank must be 16-byte aligned");
-    if (!aligned(out_ids, 4) || (out_scores && !aligned(out_scores, 4)))
-        return fail(IS_ERR_INVALID, "out_ids/out_scores must be 4-byte aligned");
     const size_t need = retrieve_need(n, d, k, nq, bank_stride, dtype);
     if (!workspace || workspace_bytes < need)
         return fail(IS_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need,
@@ -320,6 +359,27 @@ int is_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t d, i
 
     return enqueue_retrieve(query_emb, bank, n, d, k, out_ids, out_scores, nq, bank_stride, dtype,
                             workspace, (hipStream_t)stream);
+}
+
+int is_retrieve_noalloc(const void* query_emb, const void* bank, int64_t n, int32_t d, int32_t k,
+                        int32_t* out_ids, float* out_scores, int32_t nq, int64_t bank_stride,
+                        int32_t dtype, void* stream) {
+    const int rc = check_retrieve_args(query_emb, bank, n, d, k, out_ids, out_scores, nq,
+                                       bank_stride, dtype);
+    if (rc) return rc;
+    const size_t need = retrieve_need(n, d, k, nq, bank_stride, dtype);
+    if (need > kNoAllocScratchBytes)
+        return fail(IS_ERR_WORKSPACE,
+                    "these sizes need %zu bytes of scratch; is_retrieve_noalloc has %zu "
+                    "(IS_RETRIEVE_NOALLOC_MAX_BYTES): call is_retrieve with a workspace",
+                    need, kNoAllocScratchBytes);
+    hipError_t e;
+    void* ws = noalloc_scratch(&e);
+    if (!ws) return fail(IS_ERR_HIP, "scratch address lookup: %s", hipGetErrorString(e));
+    // every retrieval kernel writes the scratch it later reads: nothing in it
+    // has to start at zero
+    return enqueue_retrieve(query_emb, bank, n, d, k, out_ids, out_scores, nq, bank_stride, dtype,
+                            ws, (hipStream_t)stream);
 }
 
 int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,

@@ -271,3 +271,38 @@ def test_ann_workspace_sizes_are_pure_host():
     assert isl.is_ann_search_workspace_size(1024, 1024, 64, 256, isl.IS_DTYPE_BF16) >= 256 * 64 * 8
     with pytest.raises(isl.InferScaleError):
         isl.is_ann_build_workspace_size(10, 64, 10, isl.IS_DTYPE_F32)
+
+
+def _noalloc(**kw):
+    a = dict(q=A, bank=A, n=1000, d=64, k=10, ids=A, scores=A, nq=1, stride=0, dt=0,
+             stream=None)
+    a.update(kw)
+    lib = isl.load_library()
+    return lib.is_retrieve_noalloc(a["q"], a["bank"], a["n"], a["d"], a["k"], a["ids"],
+                                   a["scores"], a["nq"], a["stride"], a["dt"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), isl.IS_ERR_INVALID),
+    (dict(ids=None), isl.IS_ERR_INVALID),
+    (dict(k=0), isl.IS_ERR_INVALID),
+    (dict(d=60), isl.IS_ERR_INVALID),
+    (dict(dt=7), isl.IS_ERR_UNSUPPORTED),
+    (dict(stride=12), isl.IS_ERR_INVALID),
+    (dict(bank=A + 8), isl.IS_ERR_INVALID),
+    # scores alone need nq * n * 4 bytes: beyond the fixed 16 MiB array
+    (dict(n=5_000_000), isl.IS_ERR_WORKSPACE),
+    (dict(n=100_000, nq=64), isl.IS_ERR_WORKSPACE),
+])
+def test_retrieve_noalloc_rejects_on_host(kw, code):
+    assert _noalloc(**kw) == code
+    assert isl.load_library().is_last_error()
+
+
+def test_retrieve_noalloc_limit_message_names_the_sizes():
+    assert _noalloc(n=5_000_000) == isl.IS_ERR_WORKSPACE
+    msg = isl.load_library().is_last_error().decode()
+    assert "is_retrieve_noalloc" in msg and str(isl.IS_RETRIEVE_NOALLOC_MAX_BYTES) in msg
+    # the workspace is_retrieve would need is the figure it reports
+    need = isl.is_retrieve_workspace_size(5_000_000, 64, 10, 1, 0)
+    assert str(need) in msg
