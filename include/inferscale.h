@@ -326,6 +326,19 @@ int is_paged_scores(const void* q, const int32_t* qpos, const void* paged_k, int
                     void* stream);
 
 /*
+ * is_stream_copy -- dst[0 .. bytes) = src[0 .. bytes), a streaming copy of
+ * device memory (every byte read once and written once, non-temporal
+ * 16-byte accesses, all CUs sweeping the buffers together). Not a step of
+ * the method: the measured rate of this copy is the practical HBM ceiling
+ * the inject's traffic (§3.5: every stored byte of the chosen facts read
+ * once, every page byte written once) is reported against.
+ *
+ *   dst, src   device pointers, 16-byte aligned, not overlapping
+ *   bytes      a multiple of 16 (0: nothing is enqueued)
+ */
+int is_stream_copy(void* dst, const void* src, size_t bytes, void* stream);
+
+/*
  * Graph-ANN retrieval: the paper's vector backend is a GPU-resident
  * proximity graph over the fact embeddings, answered by a beam search on the
  * device (§2.6; §6.1: inner product, 64 neighbours, beam width 64). The

@@ -46,7 +46,7 @@ IS_ANN_MAX_WIDTH = 4
 IS_ANN_MAX_EXPAND = 256
 
 EXPORTED = ("is_version", "is_last_error", "is_retrieve_workspace_size", "is_retrieve",
-            "is_retrieve_noalloc", "is_slot_map", "is_inject", "is_inject_rotary", "is_place_inject", "is_paged_scores",
+            "is_retrieve_noalloc", "is_slot_map", "is_stream_copy", "is_inject", "is_inject_rotary", "is_place_inject", "is_paged_scores",
             "is_ann_build_workspace_size", "is_ann_build", "is_ann_search_workspace_size",
             "is_ann_search")
 
@@ -81,6 +81,8 @@ def load_library() -> ctypes.CDLL:
     lib.is_retrieve.restype = ctypes.c_int
     lib.is_retrieve_noalloc.argtypes = [P, P, i64, i32, i32, P, P, i32, i64, i32, P]
     lib.is_retrieve_noalloc.restype = ctypes.c_int
+    lib.is_stream_copy.argtypes = [P, P, sz, P]
+    lib.is_stream_copy.restype = ctypes.c_int
     lib.is_slot_map.argtypes = [P, P, i32, P, i32, P, P, P, i32, i32, i64, i64, i32, i32, i32, P, P]
     lib.is_slot_map.restype = ctypes.c_int
     lib.is_inject.argtypes = [P, P, P, P, P, f32, P, P, P, P, P, i32, i32, i64, i64, i32, i32,
@@ -266,6 +268,15 @@ def is_retrieve_noalloc(query_emb, bank, n, d, k, out_ids, out_scores=None, *, n
         _arg(out_ids, "out_ids", _I32, nq * k),
         _arg(out_scores, "out_scores", _F32, nq * k, optional=True), nq, bank_stride,
         dt, _stream(stream))
+
+
+def is_stream_copy(dst, src, stream=None) -> None:
+    """dst[:] = src[:] by the library's streaming copy (equal byte sizes; see
+    include/inferscale.h)."""
+    nb = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nb:
+        raise ValueError("dst and src must hold the same number of bytes")
+    _call("is_stream_copy", _Ptr(dst, False), _Ptr(src, False), nb, _stream(stream))
 
 
 def is_slot_map(ids, fact_lens, start_pos, block_table, page_size, out_slots, out_positions,

@@ -12,7 +12,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libinferscale.so")
-SOURCES = ["abi.hip", "retrieve.hip", "place.hip", "inject.hip", "consumer.hip", "ann.hip"]
+SOURCES = ["abi.hip", "retrieve.hip", "place.hip", "inject.hip", "consumer.hip", "ann.hip",
+           "copy.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

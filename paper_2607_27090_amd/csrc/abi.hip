@@ -382,6 +382,20 @@ int is_retrieve_noalloc(const void* query_emb, const void* bank, int64_t n, int3
                             ws, (hipStream_t)stream);
 }
 
+int is_stream_copy(void* dst, const void* src, size_t bytes, void* stream) {
+    if (bytes == 0) return ok();
+    if (!dst || !src) return fail(IS_ERR_INVALID, "dst and src must be non-NULL");
+    if (!aligned(dst, 16) || !aligned(src, 16) || bytes % 16)
+        return fail(IS_ERR_INVALID, "dst and src must be 16-byte aligned and bytes=%zu a multiple "
+                    "of 16", bytes);
+    const uintptr_t d0 = (uintptr_t)dst, s0 = (uintptr_t)src;
+    if (d0 < s0 + bytes && s0 < d0 + bytes)
+        return fail(IS_ERR_INVALID, "dst and src overlap");
+    const hipError_t e = is::launch_stream_copy(dst, src, (int64_t)(bytes / 16), (hipStream_t)stream);
+    if (e != hipSuccess) return fail(IS_ERR_HIP, "copy launch: %s", hipGetErrorString(e));
+    return ok();
+}
+
 int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
                 const int32_t* block_table, int32_t page_size, int64_t* out_slots,
                 int32_t* out_positions, int32_t* out_m, int32_t k, int32_t nq, int64_t n,

@@ -70,6 +70,9 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
                          int32_t interleaved, uint32_t* status, hipStream_t st,
                          const PlaceArgs* place = nullptr);
 
+// copy.hip: dst[i] = src[i] for i < units 16-byte units (non-temporal)
+hipError_t launch_stream_copy(void* dst, const void* src, int64_t units, hipStream_t st);
+
 // consumer.hip
 int consumer_max_q_elems();
 int consumer_max_group();

@@ -306,3 +306,17 @@ def test_retrieve_noalloc_limit_message_names_the_sizes():
     # the workspace is_retrieve would need is the figure it reports
     need = isl.is_retrieve_workspace_size(5_000_000, 64, 10, 1, 0)
     assert str(need) in msg
+
+
+@pytest.mark.parametrize("dst,src,nbytes", [
+    (None, A, 64), (A, None, 64), (A + 8, 2 * A, 64), (A, 2 * A + 4, 64), (A, 2 * A, 65),
+    (A, A + 32, 64),  # overlapping
+])
+def test_stream_copy_rejects(dst, src, nbytes):
+    lib = isl.load_library()
+    assert lib.is_stream_copy(dst, src, nbytes, None) == isl.IS_ERR_INVALID
+    assert lib.is_last_error()
+
+
+def test_stream_copy_of_nothing_enqueues_nothing():
+    assert isl.load_library().is_stream_copy(None, None, 0, None) == isl.IS_OK
