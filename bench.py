@@ -302,22 +302,27 @@ def main():
     # Before each step (untimed) 1 GiB of writes evicts the bank, the
     # placement arrays and any page lines from the Infinity Cache and the
     # L2s, as the model's own layers would between two requests of a serving
-    # engine; a synchronize and an event pair bracket each step. `value` is
-    # the median step.
+    # engine. The flushes and steps are enqueued back to back (the host runs
+    # ahead of the GPU, as an engine's does, so no launch waits for Python);
+    # an event pair brackets each step and one synchronize ends the region.
+    # `value` is the median step.
     cold = []
     if not args.no_cold:
         flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         cold_ret = []
+        evs = []
+        torch.cuda.synchronize()
         for i in range(args.warmup, nsteps):
             flush.fill_(i & 0xFF)
-            torch.cuda.synchronize()
             a, m_, b = (torch.cuda.Event(enable_timing=True) for _ in range(3))
             a.record()
             retrieve(queries[i], buf)
             m_.record()
             after_retrieve(i, buf)
             b.record()
-            torch.cuda.synchronize()
+            evs.append((a, m_, b))
+        torch.cuda.synchronize()
+        for a, m_, b in evs:
             cold.append(a.elapsed_time(b))
             cold_ret.append(a.elapsed_time(m_))
         del flush
@@ -637,8 +642,8 @@ def main():
         "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
                         if args.detail else None),
         "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
-        "timing": ("value and ms_per_step: median of the K steps, each timed alone from cold "
-                   "caches (1 GiB of writes before it)" if cold else
+        "timing": ("value and ms_per_step: median of the K steps, each from cold caches "
+                   "(1 GiB of writes enqueued before it, untimed)" if cold else
                    "value and ms_per_step: K steps back to back (warm caches)"),
         "cold_us_per_request": cold_pct,
         "cold_retrieve_us_per_step_median": (round(statistics.median(cold_ret) * 1e3, 2)
