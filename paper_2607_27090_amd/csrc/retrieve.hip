@@ -52,6 +52,27 @@ __device__ __forceinline__ float wave_multi_sum(float (&a)[V], int lane, int* wh
     return v;
 }
 
+// s + <a, b> over one 16-byte unit of each operand. fp32: a fused
+// multiply-add chain, then added to s. bf16: v_dot2_f32_bf16 steps
+// continuing the running sum (the two bf16 x bf16 products of a step are
+// exact; each step adds them to the fp32 sum with one rounding), a third of
+// the instructions of unpacking and multiplying element by element.
+__device__ __forceinline__ float dot16_acc(uint4 a, uint4 b, float s, F32Tag) {
+    return s + dot16(a, b, F32Tag{});
+}
+__device__ __forceinline__ float dot16_acc(uint4 a, uint4 b, float s, BF16Tag) {
+    typedef __bf16 bf16x2_t2 __attribute__((ext_vector_type(2)));
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t2, a.x),
+                                        __builtin_bit_cast(bf16x2_t2, b.x), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t2, a.y),
+                                        __builtin_bit_cast(bf16x2_t2, b.y), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t2, a.z),
+                                        __builtin_bit_cast(bf16x2_t2, b.z), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t2, a.w),
+                                        __builtin_bit_cast(bf16x2_t2, b.w), s, false);
+    return s;
+}
+
 // One block = 4 waves. blockIdx.y selects a group of NQB queries (shared
 // bank) or one query and its own bank (per-query banks, NQB == 1).
 template <class Tag, int CPL, int NQB, int RB>
@@ -93,7 +114,7 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ que
             for (int rb = 0; rb < RB; ++rb) {
                 float s = 0.f;
 #pragma unroll
-                for (int c = 0; c < CPL; ++c) s += dot16(v[rb][c], qr[qq][c], Tag{});
+                for (int c = 0; c < CPL; ++c) s = dot16_acc(v[rb][c], qr[qq][c], s, Tag{});
                 part[qq * RB + rb] = s;
             }
         int which;
@@ -112,8 +133,11 @@ static hipError_t launch_scan_t(const void* query, const void* bank, int64_t n, 
                                 int64_t bank_stride_chunks, float* scores, hipStream_t st) {
     constexpr int RB = (CPL <= 2) ? 4 : (CPL <= 4 ? 2 : 1);
     const int groups = bank_stride_chunks ? nq : (nq + NQB - 1) / NQB;
-    // aim for >= ~2048 blocks in flight over the whole grid
-    int64_t rpb = (n * groups + 2047) / 2048;
+    // aim for ~2048 blocks over the whole grid; ~512 when a row load serves
+    // 4 or 8 queries (fewer, longer-running waves keep fewer rows in flight
+    // per CU, which streams faster: 70B shape, 8 queries, 23% less time)
+    const int64_t target = NQB >= 4 ? 512 : 2048;
+    int64_t rpb = (n * groups + target - 1) / target;
     rpb = ((rpb + 4 * RB - 1) / (4 * RB)) * (4 * RB);
     if (rpb < 4 * RB) rpb = 4 * RB;
     if (rpb > 1024) rpb = 1024;

@@ -200,8 +200,10 @@ class Instance:
         li = torch.from_numpy(ll).cuda()
         si = torch.from_numpy(src).cuda()
         di = torch.from_numpy(slots).cuda()
-        kin = u16(self.store["preK"][li, si]).reshape(-1, H * D)
-        vin = u16(self.store["V"][li, si]).reshape(-1, H * D)
+        # (a host-resident store is indexed on the host)
+        sd = self.store["preK"].device
+        kin = u16(self.store["preK"][li.to(sd), si.to(sd)]).reshape(-1, H * D)
+        vin = u16(self.store["V"][li.to(sd), si.to(sd)]).reshape(-1, H * D)
         gk = u16(self.pk[li, di]).reshape(-1, H * D)
         gv = u16(self.pv[li, di]).reshape(-1, H * D)
         assert np.array_equal(gv, vin), "V rows differ"

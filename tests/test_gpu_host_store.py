@@ -68,3 +68,30 @@ def test_pageable_host_store_is_rejected_before_launch():
     torch.cuda.synchronize()
     assert rc == IS_ERR_INVALID
     assert b"preK" in lib.is_last_error()
+
+
+def test_host_store_at_the_llama_k50_shape_sampled_against_oracle():
+    # the bench's host-store configuration: Llama-3.1-8B KV shapes, 10,000
+    # facts aliased onto 2,048 payloads in pinned host memory (~10.5 GB), one
+    # request with k=50 placed and injected in one launch over PCIe; checked
+    # against the oracle on sampled rows (1% plus every fact's first and last
+    # token) and, bit for bit, against the same request from a device store
+    w = workloads.LLAMA8B.with_(payloads=2048)
+    host = workloads.make_store(w, "cuda", host=True)
+    a = Instance(w, store=host)
+    a.run(fused=True)
+    near = a.check_retrieve()
+    a.check_slot_map()
+    rows, floor = a.check_inject_sampled(frac=0.01, seed=5)
+    pk_host, pv_host = a.pk.clone(), a.pv.clone()
+    del host
+    dev = workloads.make_store(w, "cuda")
+    b = Instance(w, store=dev, bank=a.bank)
+    b.run(fused=True)
+    assert torch.equal(a.buf.ids, b.buf.ids) and torch.equal(a.buf.slots, b.buf.slots)
+    assert torch.equal(pk_host.view(torch.int16), b.pk.view(torch.int16))
+    assert torch.equal(pv_host.view(torch.int16), b.pv.view(torch.int16))
+    log(f"host store at k=50: m={int(a.buf.m.sum())} tokens, near-tie swaps {near}, {rows} "
+        f"sampled rows against the oracle (floor-rescued {floor}), pages equal to the "
+        f"device-store run")
+
