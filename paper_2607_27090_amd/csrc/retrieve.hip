@@ -488,7 +488,6 @@ constexpr int kSelKpt = 16;
 constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kSelCap = 2048;      // candidates kept in shared memory
 constexpr int kSelRankMax = 512;   // largest candidate set ranked pairwise
-constexpr int kSelWaveRanks = 8;   // single-chunk select: per-wave bound for want <= 16 * 8
 
 struct SelShared {
     uint64_t cand[kSelCap];
@@ -789,24 +788,16 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 //    are gathered in LDS (each wave reserves its run with one atomic) and
 //    ranked pairwise. Should there be more than kSelRankMax of them (many
 //    tied scores), the general select over 64-bit keys takes over.
-// Shared memory of the single-chunk select.
-struct SelSmallShared {
-    SelShared sh;
-    uint32_t hist2[256];   // radix passes alternate between sh.hist and this
-    uint32_t ncand;
-};
-
-// The single-chunk select of one query, by every thread of a kSelThreads
-// block: sq[0 .. M) are its scores; the k winners go to out_ids[0 .. k) and
-// out_scores[0 .. k) (may be NULL).
 template <int KPT>
-__device__ void select_small_block(const float* __restrict__ sq, int64_t M, int k,
-                                   int32_t* __restrict__ out_ids, float* __restrict__ out_scores,
-                                   SelSmallShared& ss) {
-    SelShared& sh = ss.sh;
-    uint32_t* s_hist2 = ss.hist2;
-    uint32_t& s_ncand = ss.ncand;
+__global__ __launch_bounds__(kSelThreads) void select_small_kernel(
+    const float* __restrict__ scores, int64_t M, int k, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_scores) {
+    __shared__ SelShared sh;
+    __shared__ uint32_t s_hist2[256];   // radix passes alternate between sh.hist and this
+    __shared__ uint32_t s_ncand;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int q = blockIdx.y;
+    const float* sq = scores + (int64_t)q * M;
     uint32_t u[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
@@ -820,28 +811,7 @@ __device__ void select_small_block(const float* __restrict__ sq, int64_t M, int 
 
     // ---- 1. lower bound tau on the score bits ----
     uint32_t tau = 0;  // every valid key is a candidate
-    // per-wave bound (one barrier): when every thread holds a valid key and
-    // want <= kSelWaves * kSelWaveRanks, each wave takes the c-th largest of
-    // its 64 thread maxima, c = ceil(want / kSelWaves); the smallest of
-    // those, tau, has at least kSelWaves * c >= want distinct keys >= it
-    const int c_per_wave = (want + kSelWaves - 1) / kSelWaves;
-    if ((int64_t)want < M && M >= kSelThreads && c_per_wave <= kSelWaveRanks) {
-        uint32_t x = 0;
-#pragma unroll
-        for (int i = 0; i < KPT; ++i) x = (i < nv && u[i] > x) ? u[i] : x;
-        uint32_t tw = 0;
-        for (int r = 0; r < c_per_wave; ++r) {
-            tw = wave_max_u32(x);
-            // take one lane holding the maximum out of the next round
-            const uint64_t hold = __ballot(x == tw);
-            if (lane == (int)__builtin_ctzll(hold)) x = 0;
-        }
-        if (lane == 0) sh.group[wave] = tw;
-        __syncthreads();
-        tau = 0xFFFFFFFFu;
-#pragma unroll
-        for (int w = 0; w < kSelWaves; ++w) tau = min(tau, (uint32_t)sh.group[w]);
-    } else if ((int64_t)want < M) {
+    if ((int64_t)want < M) {
         uint32_t tm = 0;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) tm = (i < nv && u[i] > tm) ? u[i] : tm;
@@ -969,19 +939,9 @@ __device__ void select_small_block(const float* __restrict__ sq, int64_t M, int 
     // ---- output, best first ----
     for (int i = t; i < got; i += kSelThreads) {
         const uint64_t me = sh.sel[i];
-        out_ids[i] = (int32_t)key_id(me);
-        if (out_scores) out_scores[i] = key_score(me);
+        out_ids[(int64_t)q * k + i] = (int32_t)key_id(me);
+        if (out_scores) out_scores[(int64_t)q * k + i] = key_score(me);
     }
-}
-
-template <int KPT>
-__global__ __launch_bounds__(kSelThreads) void select_small_kernel(
-    const float* __restrict__ scores, int64_t M, int k, int32_t* __restrict__ out_ids,
-    float* __restrict__ out_scores) {
-    __shared__ SelSmallShared ss;
-    const int64_t q = blockIdx.y;
-    select_small_block<KPT>(scores + q * M, M, k, out_ids + q * k,
-                            out_scores ? out_scores + q * k : nullptr, ss);
 }
 
 // Final ranking of the filtered matrix-core scan, one block per query. The
