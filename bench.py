@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--detail", action="store_true",
                     help="also time one stream (latency) and each call separately")
     ap.add_argument("--graph", action="store_true", help="also time the request as a HIP graph")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor GEMM (torch.matmul, bf16) on the same shared bank "
+                         "and one step's queries, as a yardstick for the matrix-core scan")
     ap.add_argument("--no-two-streams", action="store_true",
                     help="skip the two-stream throughput figure (its kernels overlap, which "
                          "per-kernel profiles should not average in)")
@@ -99,6 +102,9 @@ def parse():
                     help="kernel name fragment the summary is about (default: the inject "
                          "kernel of the run's path)")
     ap.add_argument("--title", default="", help="title line of the summary")
+    ap.add_argument("--include", action="append", default=[],
+                    help="kernel name fragment to list besides the library's own kernels "
+                         "(repeatable), e.g. the vendor GEMM of --library-gemm")
     ap.add_argument("--cmd", action="append", default=[],
                     help="command that produced the profile (repeatable), quoted in the summary")
     return ap.parse_args()
@@ -518,6 +524,30 @@ def main():
     log(f"inject: mean m={statistics.fmean(m_steps):.0f} tokens/step, "
         f"{statistics.fmean(inj_bytes) / 1e6:.1f} MB/step, {achieved:.0f} GB/s per launch")
 
+    # ---- optional: the vendor GEMM on the same bank and queries -----------------
+    # (dense scores [n][nq] in bf16, no top-k: a yardstick for the scan alone)
+    library_gemm = None
+    if args.library_gemm and w.shared_bank and bank.dtype == torch.bfloat16:
+        qt = queries[args.warmup].reshape(w.nq, w.d_e).t().contiguous()
+        bank2 = bank.reshape(w.n, w.d_e)
+        gout = torch.empty(w.n, w.nq, dtype=torch.bfloat16, device=dev)
+        for _ in range(3):
+            torch.matmul(bank2, qt, out=gout)
+        ge = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+        for j in range(args.steps):
+            ge[2 * j].record()
+            torch.matmul(bank2, qt, out=gout)
+            ge[2 * j + 1].record()
+        torch.cuda.synchronize()
+        g_ms = statistics.median(ge[2 * j].elapsed_time(ge[2 * j + 1]) for j in range(args.steps))
+        library_gemm = {"what": "torch.matmul(bank [n][d], queries^T [d][nq]) -> bf16 [n][nq]",
+                        "us_median": round(g_ms * 1e3, 1),
+                        "TFLOPs": round(scan_flop / (g_ms * 1e-3) / 1e12, 1),
+                        "bank_GBps": round(scan_bytes / (g_ms * 1e-3) / 1e9, 1)}
+        del gout
+        log(f"library GEMM on the same bank: {library_gemm['us_median']} us, "
+            f"{library_gemm['TFLOPs']} TFLOP/s")
+
     # ---- optional: the same request captured as a HIP graph --------------------
     graph_us = None
     if args.graph and nwaves == 1:
@@ -656,6 +686,7 @@ def main():
             "us": round(ret_ms * 1e3, 2), "bank_bytes": scan_bytes,
             "GBps": round(scan_bytes / (ret_ms * 1e-3) / 1e9, 1),
             "TFLOPs": round(scan_flop / (ret_ms * 1e-3) / 1e12, 2)},
+        "library_gemm": library_gemm,
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "copy_ceiling": {
             "kernel": "is_stream_copy (non-temporal 16-byte grid-stride copy)",
@@ -837,8 +868,10 @@ def summarize_stats(args):
              "|---|---:|---:|---:|---:|---:|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
         name = _short_kernel(r["Name"])
-        if not name.startswith("is::"):
+        if not name.startswith("is::") and not any(f in r["Name"] for f in args.include):
             continue
+        if len(name) > 90:
+            name = name[:87] + "..."
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['Percentage']):.1f}% |")
@@ -847,6 +880,11 @@ def summarize_stats(args):
               f"({meta.get('timing', '')}), warm {meta.get('warm_us_per_request')} us/request, "
               f"inject launch {meta.get('inject_launch_us')} us event-timed, "
               f"{roof.get('achieved')} GB/s = {roof.get('frac')} of {roof.get('peak')} GB/s."]
+    if meta.get("library_gemm"):
+        g = meta["library_gemm"]
+        lines += ["", f"Vendor GEMM on the same bank and queries ({g['what']}): "
+                  f"{g['us_median']} us event-timed median, {g['TFLOPs']} TFLOP/s, "
+                  f"bank read at {g['bank_GBps']} GB/s."]
     return "\n".join(lines)
 
 
