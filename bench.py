@@ -311,29 +311,39 @@ def main():
     # engine. The flushes and steps are enqueued back to back (the host runs
     # ahead of the GPU, as an engine's does, so no launch waits for Python);
     # an event pair brackets each step and one synchronize ends the region.
-    # `value` is the median step.
-    cold = []
+    # `value` is the median step. A second pass of the same cold steps puts a
+    # third event between the retrieval and the inject, for the retrieval's
+    # share; it is kept out of the first pass because an event recorded
+    # between two kernels holds the second one back by a few microseconds
+    # (cold_split_pass_us_per_step_median shows by how much).
+    cold, cold_ret, cold_split = [], [], []
     if not args.no_cold:
         flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        cold_ret = []
-        evs = []
-        torch.cuda.synchronize()
-        for i in range(args.warmup, nsteps):
-            flush.fill_(i & 0xFF)
-            a, m_, b = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-            a.record()
-            retrieve(queries[i], buf)
-            m_.record()
-            after_retrieve(i, buf)
-            b.record()
-            evs.append((a, m_, b))
-        torch.cuda.synchronize()
-        for a, m_, b in evs:
-            cold.append(a.elapsed_time(b))
-            cold_ret.append(a.elapsed_time(m_))
+        for split in (False, True):
+            evs = []
+            torch.cuda.synchronize()
+            for i in range(args.warmup, nsteps):
+                flush.fill_(i & 0xFF)
+                a, m_, b = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+                a.record()
+                retrieve(queries[i], buf)
+                if split:
+                    m_.record()
+                after_retrieve(i, buf)
+                b.record()
+                evs.append((a, m_, b))
+            torch.cuda.synchronize()
+            for a, m_, b in evs:
+                if split:
+                    cold_ret.append(a.elapsed_time(m_))
+                    cold_split.append(a.elapsed_time(b))
+                else:
+                    cold.append(a.elapsed_time(b))
         del flush
         log(f"cold: median {statistics.median(cold) * 1e3 / w.nq:.2f} us/request over "
-            f"{len(cold)} steps")
+            f"{len(cold)} steps (with an event after the retrieval: "
+            f"{statistics.median(cold_split) * 1e3 / w.nq:.2f}, retrieval "
+            f"{statistics.median(cold_ret) * 1e3:.2f} us/step)")
     ms_per_step = statistics.median(cold) if cold else warm_ms_per_step
 
     def pcts(xs):
@@ -678,6 +688,8 @@ def main():
         "cold_us_per_request": cold_pct,
         "cold_retrieve_us_per_step_median": (round(statistics.median(cold_ret) * 1e3, 2)
                                              if cold else None),
+        "cold_split_pass_us_per_step_median": (round(statistics.median(cold_split) * 1e3, 2)
+                                               if cold else None),
         "warm_us_per_request": round(warm_ms_per_step * 1e3 / w.nq, 3),
         "warm_us_per_request_percentiles": latency_pct,
         "graph_step_us_median": None if graph_us is None else round(graph_us, 2),
