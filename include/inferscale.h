@@ -219,9 +219,9 @@ int is_slot_map(const int32_t* ids, const int32_t* fact_lens, int32_t start_pos,
  * Tokens whose slot lies outside [0, num_slots) and facts whose rows fall
  * outside the store are skipped and flagged.
  * Launch footprint: max(1, CUs / nq) workgroups of 768 threads per request,
- * each reserving 84 KiB of LDS so that it has its CU to itself; kernels on
- * other streams can share those CUs only within the remaining LDS and
- * registers.
+ * each holding just over half of its CU's LDS (81 KiB of 160 KiB on MI355X)
+ * so that it has its CU to itself; kernels on other streams can share those
+ * CUs within the other half of the LDS and the remaining registers.
  */
 int is_inject(const int32_t* ids, const void* preK, const void* V, const int64_t* slots,
               const int32_t* positions, float rope_theta, void* paged_k, void* paged_v,

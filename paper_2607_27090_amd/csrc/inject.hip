@@ -53,9 +53,10 @@ namespace is {
 constexpr int kInjThreads = 768;
 constexpr int kInjFacts = 2;       // consecutive facts of the placement per thread in set-up
 constexpr int kInjLayers = 1;      // layers of one work item (2 and 4 measured slower)
-// dynamic LDS requested beyond the kernel's own, so that no two workgroups
-// share a CU (160 KiB of LDS per CU)
-constexpr size_t kInjLdsReserve = 84 * 1024;
+// The launch asks for just enough dynamic LDS that the kernel's static and
+// dynamic LDS together exceed half of a CU's (80 KiB of 160 KiB on MI355X):
+// no two of its workgroups then share a CU, and the other half stays free
+// for kernels on other streams.
 // block-table entries each thread loads with the fact ids (PLACE); blocks
 // beyond 2 * 1024 are read after the scan
 constexpr int kInjBtAhead = 2;
@@ -441,26 +442,43 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     if (per_req > items_max) per_req = items_max;
     if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
-    // allow the dynamic LDS reserve (once per device; setting it twice from
-    // racing threads is harmless)
-    static std::atomic<bool> lds_attr_set[64];
+    // the dynamic LDS reserve and its attribute, once per device (racing
+    // threads compute and set the same values)
+    static std::atomic<int> lds_reserve[64];
     int dev = 0;
-    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 &&
-        !lds_attr_set[dev].load(std::memory_order_acquire)) {
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const bool cached = dev >= 0 && dev < 64;
+    int reserve = cached ? lds_reserve[dev].load(std::memory_order_acquire) : 0;
+    if (reserve == 0) {
+        int lds_per_cu = 0;
+        e = hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  dev);
+        if (e != hipSuccess) return e;
         const void* fns[4] = {(const void*)inject_kernel<false, false>,
                               (const void*)inject_kernel<true, false>,
                               (const void*)inject_kernel<false, true>,
                               (const void*)inject_kernel<true, true>};
+        size_t static_lds = 0;
         for (const void* fn : fns) {
-            const hipError_t e = hipFuncSetAttribute(
-                fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kInjLdsReserve);
+            hipFuncAttributes attr;
+            e = hipFuncGetAttributes(&attr, fn);
+            if (e != hipSuccess) return e;
+            if (attr.sharedSizeBytes > static_lds) static_lds = attr.sharedSizeBytes;
+        }
+        // total > half, in whole KiB; at least 1 KiB so that the value also
+        // marks the device as done
+        const int64_t need = (int64_t)lds_per_cu / 2 + 1024 - (int64_t)static_lds;
+        reserve = (int)((need < 1024 ? 1024 : need + 1023) / 1024 * 1024);
+        for (const void* fn : fns) {
+            e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, reserve);
             if (e != hipSuccess) return e;
         }
-        lds_attr_set[dev].store(true, std::memory_order_release);
+        if (cached) lds_reserve[dev].store(reserve, std::memory_order_release);
     }
     const PlaceArgs pl = place ? *place : PlaceArgs{};
 #define IS_LAUNCH_INJECT(IL, PLACE)                                                                \
-    hipLaunchKernelGGL((inject_kernel<IL, PLACE>), grid, dim3(kInjThreads), kInjLdsReserve, st,   \
+    hipLaunchKernelGGL((inject_kernel<IL, PLACE>), grid, dim3(kInjThreads), (size_t)reserve, st, \
                        ids, (const uint4*)preK, (const uint4*)V, slots, positions, rope_theta,     \
                        (uint4*)paged_k, (uint4*)paged_v, fact_offsets, fact_lens, m, k, n,         \
                        lens_stride, reverse_rank, max_tokens, L, H, D, T_store, num_slots,         \
