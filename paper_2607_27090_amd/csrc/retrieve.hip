@@ -3,17 +3,24 @@
 // graph index).
 //
 // Two stages:
-//  1. scan: s_j = <q, e_j> for every bank row. Bandwidth-bound GEMV: each
-//     wave streams whole rows with 16-byte loads, keeps its queries in
-//     registers, and reduces per-row partial sums across the wave with a
-//     transposing butterfly so that V partial sums cost V-1 shuffles.
+//  1. scan: s_j = <q, e_j> for every bank row, by one of
+//     * scan_kernel, a bandwidth-bound GEMV: each wave streams whole rows
+//       with 16-byte loads, keeps its 1-8 queries in registers and reduces
+//       the per-row partial sums across the wave with a transposing
+//       butterfly, so that V partial sums cost V-1 shuffles;
+//     * scan_mfma_kernel (32 or more queries against one bf16 bank):
+//       256-row x 256-query tiles of v_mfma_f32_32x32x16_bf16 with both
+//       operands staged through LDS, writing every score or only those not
+//       below a per-query threshold.
 //  2. select: the k largest 64-bit rank keys (score bits, ~id) per query.
-//     One 1024-thread workgroup owns a chunk of up to 16384 keys in
-//     registers, bounds the answer from below by the per-wave c-th largest
-//     keys, and radix-selects among the few keys above that bound (8-bit
-//     digits from the highest differing bit). Chunks emit k candidates each;
-//     a final pass over the candidates orders the winners (score desc,
-//     id asc).
+//     A 1024-thread workgroup holds up to 16384 keys in registers, bounds
+//     the answer from below (the smallest of k group maxima; for one chunk
+//     of fp32 scores, a radix bracket of the thread maxima), gathers the
+//     few keys above the bound and ranks them pairwise (a radix select
+//     takes over when many keys tie). Larger inputs go in chunks whose k
+//     winners a final pass ranks; the survivors of the filtered
+//     matrix-core scan are ranked by select_regions_kernel. Ties go to the
+//     lower id (score desc, id asc).
 #include "wave.hpp"
 #include "launch.hpp"
 
@@ -740,19 +747,6 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     }
 }
 
-// Final top-k of at most kSelThreads * KPT fp32 scores per query, one block
-// per query (the single-chunk case: one query against a bank of up to 16,384
-// facts). Work is kept small because one CU does all of it:
-//  * thresholds are taken on the 32-bit order-preserving images of the
-//    scores (the id only breaks ties, so it is attached to candidates only);
-//  * the lower bound tau is the lower edge of a narrow bin holding the
-//    want-th largest thread maximum: radix passes of 8 bits over the thread
-//    maxima, from the highest bit where they differ, until at most 32 of them
-//    share the bin; at least `want` scores are >= tau and typically few more;
-//  * the candidates (valid, score bits >= tau) get their 64-bit rank keys,
-//    are compacted with wave ballots and ranked pairwise. Should there be
-//    more than kSelRankMax of them (many tied scores), the general select
-//    over 64-bit keys takes over.
 // Largest / smallest value over the 64 lanes of a wave (uniform result): DPP
 // quad, half-row and row exchanges give every lane its 16-lane row's value,
 // the four rows are combined in scalar registers.
