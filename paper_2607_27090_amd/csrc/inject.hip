@@ -170,6 +170,22 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
     uint32_t flags = 0;
     int64_t flen[kInjFacts];
     int64_t len = 0;  // this thread's facts together
+    // every fact's length and store row are loaded before any is used (an
+    // id out of range reads fact 0, n >= 1, and is then dropped): loads
+    // under per-fact conditions are compiled into branches that each wait
+    // for their load, one memory round trip per load
+    int32_t lraw[kInjFacts];
+    int64_t oraw[kInjFacts];
+#pragma unroll
+    for (int f = 0; f < kInjFacts; ++f) {
+        const int64_t c = (cid[f] >= 0 && (int64_t)cid[f] < n) ? cid[f] : 0;
+        lraw[f] = lens[c];
+        oraw[f] = offs[c];
+    }
+    // (the empty asm keeps the compiler from sinking a load back into the
+    // branch that uses it)
+#pragma unroll
+    for (int f = 0; f < kInjFacts; ++f) asm volatile("" ::"v"(lraw[f]), "v"(oraw[f]));
 #pragma unroll
     for (int f = 0; f < kInjFacts; ++f) {
         const int i = kInjFacts * t + f;
@@ -179,8 +195,8 @@ __global__ __launch_bounds__(kInjThreads, 1) void inject_kernel(
             if (cid[f] < 0 || (int64_t)cid[f] >= n) {
                 flags |= IS_DEV_ID_RANGE;
             } else {
-                const int32_t l = lens[cid[f]];
-                const int64_t o = offs[cid[f]];
+                const int32_t l = lraw[f];
+                const int64_t o = oraw[f];
                 if (l < 0) {
                     flags |= IS_DEV_BAD_LEN;
                 } else {

@@ -738,18 +738,30 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
 
     uint64_t key[kSelKpt];
+    if (FROM_SCORES) {
+        // every load is issued before the first is used: an index past the
+        // end re-reads the last score (M >= 1), whose value is then dropped
+        // (a load under a per-element condition is compiled into its own
+        // branch, and each branch waits for its load)
+        float v[kSelKpt];
 #pragma unroll
-    for (int i = 0; i < kSelKpt; ++i) {
-        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
-        uint64_t kv = 0;
-        if (idx < M) {
-            if (FROM_SCORES)
-                kv = rank_key(scores[(int64_t)q * M + idx], (uint32_t)idx);
-            else
-                kv = keys_in[(int64_t)q * M + idx];
+        for (int i = 0; i < kSelKpt; ++i) {
+            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
+            v[i] = scores[(int64_t)q * M + (idx < M ? idx : M - 1)];
         }
-        key[i] = kv;  // nonzero iff valid: ~id has its top bit set for ids < 2^31
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;
+            key[i] = idx < M ? rank_key(v[i], (uint32_t)idx) : 0ull;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
+            key[i] = idx < M ? keys_in[(int64_t)q * M + idx] : 0ull;
+        }
     }
+    // key[i] is nonzero iff valid: ~id has its top bit set for ids < 2^31
     const int want = select_block(key, k, sh);
 
     // ---- output, best first ----
@@ -810,11 +822,19 @@ __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int q = blockIdx.y;
     const float* sq = scores + (int64_t)q * M;
-    uint32_t u[KPT];
+    // all loads issued before the first is used (an index past the end
+    // re-reads the last score, M >= 1, and is then dropped)
+    float sv[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
         const int64_t idx = t + (int64_t)i * kSelThreads;  // coalesced
-        u[i] = idx < M ? score_order_bits(sq[idx]) : 0u;
+        sv[i] = sq[idx < M ? idx : M - 1];
+    }
+    uint32_t u[KPT];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+        const int64_t idx = t + (int64_t)i * kSelThreads;
+        u[i] = idx < M ? score_order_bits(sv[i]) : 0u;
     }
     const int want = (int)min_i64(k, M);
     // the thread's keys are valid for i < nv (NaN scores are valid, lowest)
@@ -992,30 +1012,37 @@ __global__ __launch_bounds__(kSelThreads) void select_regions_kernel(
     uint64_t carry = 0;
     int want;
     while (true) {
+        // every slot's candidate is loaded before any is used (a slot without
+        // one re-reads fq[0], k >= 1, and drops it): loads under per-slot
+        // conditions are compiled into branches that each wait for their load
         uint64_t key[kSelKpt];
+        uint32_t have = 0;  // bit i: slot i holds a candidate
 #pragma unroll
         for (int i = 0; i < kSelKpt; ++i) {
             const int64_t slot = t + (int64_t)i * kSelThreads;
-            uint64_t kv = 0;
-            if (slot < carried) {
-                kv = carry;  // only i == 0 and t < carried
-            } else {
-                const int64_t x = next + slot - carried;
-                if (x < total) {
-                    if (x < k) {
-                        kv = fq[x];
-                    } else {
-                        const int64_t y = x - k;
-                        int lo = 0, hi = G - 1;  // last region g with s_pre[g] <= y
-                        while (lo < hi) {
-                            const int mid = (lo + hi + 1) >> 1;
-                            if (s_pre[mid] <= y) lo = mid; else hi = mid - 1;
-                        }
-                        kv = rq[(int64_t)lo * rcap + (y - s_pre[lo])];
+            const int64_t x = next + slot - carried;
+            const uint64_t* src = fq;
+            if (slot >= carried && x < total) {
+                have |= 1u << i;
+                if (x < k) {
+                    src = fq + x;
+                } else {
+                    const int64_t y = x - k;
+                    int lo = 0, hi = G - 1;  // last region g with s_pre[g] <= y
+                    while (lo < hi) {
+                        const int mid = (lo + hi + 1) >> 1;
+                        if (s_pre[mid] <= y) lo = mid; else hi = mid - 1;
                     }
+                    src = rq + (int64_t)lo * rcap + (y - s_pre[lo]);
                 }
             }
-            key[i] = kv;
+            key[i] = *src;
+        }
+#pragma unroll
+        for (int i = 0; i < kSelKpt; ++i) {
+            const int64_t slot = t + (int64_t)i * kSelThreads;
+            // a carried winner (only i == 0 and t < carried), a candidate, or empty
+            key[i] = slot < carried ? carry : ((have >> i) & 1u ? key[i] : 0ull);
         }
         next += kChunk - carried;
         want = select_block(key, k, sh);
