@@ -867,14 +867,22 @@ __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
             s_hist2[t] = 0;
         }
         __syncthreads();
-        uint32_t ref = 0, lowest = 0xFFFFFFFFu, lowest_nn = 0xFFFFFFFFu, n_nn = 0;
+        // every wave combines the 16 waves' statistics itself: lane l reads
+        // entry l of the four 16-entry tables and each 16-lane row reduces its
+        // table (max, min, min, sum) with exchanges inside the row (one LDS
+        // read per lane instead of 64)
+        static_assert(4 * kSelWaves == kWave, "four tables of one entry per wave");
+        const int row = lane >> 4;
+        uint32_t gv = (uint32_t)sh.group[lane];
 #pragma unroll
-        for (int w = 0; w < kSelWaves; ++w) {
-            ref = max(ref, (uint32_t)sh.group[w]);
-            lowest = min(lowest, (uint32_t)sh.group[kSelWaves + w]);
-            lowest_nn = min(lowest_nn, (uint32_t)sh.group[2 * kSelWaves + w]);
-            n_nn += (uint32_t)sh.group[3 * kSelWaves + w];
+        for (int off = 8; off >= 1; off >>= 1) {
+            const uint32_t o = __shfl_xor(gv, off, kWave);
+            gv = row == 0 ? max(gv, o) : (row == 3 ? gv + o : min(gv, o));
         }
+        const uint32_t ref = __builtin_amdgcn_readlane(gv, 0);
+        uint32_t lowest = __builtin_amdgcn_readlane(gv, 16);
+        const uint32_t lowest_nn = __builtin_amdgcn_readlane(gv, 32);
+        const uint32_t n_nn = __builtin_amdgcn_readlane(gv, 48);
         if (n_nn >= (uint32_t)want) lowest = lowest_nn;
         // at least `want` maxima lie in [lowest, ref]; those below are left
         // out of the histogram by the prefix test
