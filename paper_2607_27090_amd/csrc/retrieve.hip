@@ -151,10 +151,12 @@ static hipError_t launch_scan_t(const void* query, const void* bank, int64_t n, 
                                 int64_t bank_stride_chunks, float* scores, hipStream_t st) {
     constexpr int RB = (CPL <= 2) ? 4 : (CPL <= 4 ? 2 : 1);
     const int groups = bank_stride_chunks ? nq : (nq + NQB - 1) / NQB;
-    // aim for ~2048 blocks over the whole grid; ~512 when a row load serves
+    // aim for ~4096 blocks over the whole grid (at least 4 RB rows each: the
+    // 10,000-row bank of one query gets 1,250); ~512 when a row load serves
     // 4 or 8 queries (fewer, longer-running waves keep fewer rows in flight
-    // per CU, which streams faster: 70B shape, 8 queries, 23% less time)
-    const int64_t target = NQB >= 4 ? 512 : 2048;
+    // per CU, which streams faster: 70B shape, 8 queries, 23% less time).
+    // 64 per-user banks of 2,000 rows: 4,032 blocks, 3% less time than 2,048
+    const int64_t target = NQB >= 4 ? 512 : 4096;
     int64_t rpb = (n * groups + target - 1) / target;
     rpb = ((rpb + 4 * RB - 1) / (4 * RB)) * (4 * RB);
     if (rpb < 4 * RB) rpb = 4 * RB;
