@@ -124,3 +124,30 @@ def test_stats_summary_lists_the_library_kernels(tmp_path):
     assert "| `is::inject_kernel<false, true>` | 10 | 105.00 |" in r.stdout
     assert "at::native" not in r.stdout
     assert "inject launch 104.8 us" in r.stdout
+
+
+def test_stats_summary_includes_named_kernels_and_the_library_gemm(tmp_path):
+    import csv
+    d = tmp_path / "st"
+    d.mkdir()
+    long_name = "Cijk_Ailk_Bljk_BBS_BH_Bias_HA_S_SAV_UserArgs_MT256x256x64_MI16x16x1_SN_LDSB1_AFC1_AFEM1_ETC"
+    with open(d / "run_kernel_stats.csv", "w", newline="") as fh:
+        wr = csv.writer(fh)
+        wr.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs",
+                     "MaxNs", "StdDev"])
+        wr.writerow(["void is::scan_mfma_kernel<true>(int)", 5, 3000000, 600000.0, 60.0,
+                     590000, 610000, 1.0])
+        wr.writerow([long_name, 4, 2880000, 720000.0, 40.0, 700000, 740000, 1.0])
+        wr.writerow(["void at::native::fill(int)", 3, 30000, 10000.0, 1.0, 9000, 11000, 1.0])
+    (d / "bench.json").write_text(json.dumps({
+        "value": 200.0, "unit": "us/request", "inject_launch_us": 12000.0,
+        "roofline": {"achieved": 5000.0, "frac": 0.625, "peak": 8000.0},
+        "library_gemm": {"what": "torch.matmul(...)", "us_median": 814.4, "TFLOPs": 643.8,
+                         "bank_GBps": 2514.8}}) + "\n")
+    r = _run(["--summarize-stats", str(d), "--include", "Cijk", "--title", "t", "--cmd", "x"])
+    assert r.returncode == 0, r.stderr
+    assert "| `is::scan_mfma_kernel<true>` | 5 | 600.00 |" in r.stdout
+    # names past 90 characters are cut with an ellipsis
+    assert f"| `{long_name[:87]}...` | 4 | 720.00 |" in r.stdout
+    assert "at::native" not in r.stdout
+    assert "814.4 us event-timed median, 643.8 TFLOP/s" in r.stdout
