@@ -53,10 +53,6 @@ namespace is {
 constexpr int kInjThreads = 768;
 constexpr int kInjFacts = 2;       // consecutive facts of the placement per thread in set-up
 constexpr int kInjLayers = 1;      // layers of one work item (2 and 4 measured slower)
-// The launch asks for just enough dynamic LDS that the kernel's static and
-// dynamic LDS together exceed half of a CU's (80 KiB of 160 KiB on MI355X):
-// no two of its workgroups then share a CU, and the other half stays free
-// for kernels on other streams.
 // block-table entries each thread loads with the fact ids (PLACE); blocks
 // beyond 2 * 1024 are read after the scan
 constexpr int kInjBtAhead = 2;
@@ -459,7 +455,10 @@ hipError_t launch_inject(const int32_t* ids, const void* preK, const void* V, co
     if (per_req < 1) per_req = 1;
     dim3 grid((unsigned)per_req, (unsigned)nq);
     // the dynamic LDS reserve and its attribute, once per device (racing
-    // threads compute and set the same values)
+    // threads compute and set the same values): just enough that the
+    // kernel's static and dynamic LDS together exceed half of a CU's (80 KiB
+    // of 160 KiB on MI355X), so that no two of its workgroups share a CU and
+    // the other half stays free for kernels on other streams
     static std::atomic<int> lds_reserve[64];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
