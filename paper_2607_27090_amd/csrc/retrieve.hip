@@ -92,13 +92,38 @@ __device__ __forceinline__ uint4 load_stream(const uint4* p) {
 
 // One block = 4 waves. blockIdx.y selects a group of NQB queries (shared
 // bank) or one query and its own bank (per-query banks, NQB == 1).
+// Raw buffer descriptors: loads at byte offsets >= the descriptor's size
+// read zero, which pads ragged row tiles and reduction chunks for free.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family raw buffer format word
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             kRsrcWord3);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(rsrc_t r, uint32_t off) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+// The same with the non-temporal hint (cache-policy bit 1): bank rows are
+// streamed once per call (3% less time for the 1M-row scan than ordinary
+// loads); the queries, re-read for every row tile, keep ordinary loads.
+__device__ __forceinline__ uint4 buffer_load16_stream(rsrc_t r, uint32_t off, uint32_t soff = 0) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, (int)soff, 2);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+constexpr int kScanMaxRows = 1024;  // rows per block at most
+
 template <class Tag, int CPL, int NQB, int RB>
 __global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ query,
                                                    const uint4* __restrict__ bank, int64_t n,
                                                    int chunks, int nq, int64_t bank_stride_chunks,
                                                    int rows_per_block, float* __restrict__ scores) {
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform, so the row loops below are scalar control flow
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int q0 = blockIdx.y * NQB;
     const uint4* B = bank + (int64_t)blockIdx.y * bank_stride_chunks;
 
@@ -114,17 +139,12 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ que
 
     const int64_t tile0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t tile1 = min(n, tile0 + rows_per_block);
-    for (int64_t base = tile0 + (int64_t)wave * RB; base < tile1; base += 4 * RB) {
-        uint4 v[RB][CPL];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                const int ci = lane + c * kWave;
-                const int64_t row = base + rb;
-                v[rb][c] = (row < tile1 && ci < chunks) ? load_stream(B + row * chunks + ci)
-                                                        : make_uint4(0, 0, 0, 0);
-            }
+    int64_t base = tile0 + (int64_t)wave * RB;
+    constexpr int64_t kStep = 4 * RB;  // rows between a wave's batches
+
+    // sum of RB rows x NQB queries, reduced across the wave; the lanes whose
+    // low bits are zero hand (query, row offset, score) to put()
+    auto reduce_rows = [&](uint4 (&v)[RB][CPL], auto&& put) {
         float part[NQB * RB];
 #pragma unroll
         for (int qq = 0; qq < NQB; ++qq)
@@ -138,10 +158,112 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ que
         int which;
         const float tot = wave_multi_sum<NQB * RB>(part, lane, &which);
         constexpr int kLowBits = (NQB * RB >= 64) ? 0 : 6 - __builtin_ctz(NQB * RB);
-        if ((lane & ((1 << kLowBits) - 1)) == 0) {
-            const int qq = which / RB, rb = which % RB;
-            const int64_t row = base + rb;
-            if (row < tile1 && q0 + qq < nq) scores[(int64_t)(q0 + qq) * n + row] = tot;
+        if ((lane & ((1 << kLowBits) - 1)) == 0) put(which / RB, which % RB, tot);
+    };
+
+    if constexpr (NQB == 1) {
+        // One query per block (the single-query bank, per-user banks): the
+        // grid is fine-grained (a few batches per wave, many waves per CU),
+        // so each batch is loaded, reduced and stored in turn.
+        for (; base < tile1; base += kStep) {
+            uint4 v[RB][CPL];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) {
+                    const int ci = lane + c * kWave;
+                    const int64_t row = base + rb;
+                    v[rb][c] = (row < tile1 && ci < chunks) ? load_stream(B + row * chunks + ci)
+                                                            : make_uint4(0, 0, 0, 0);
+                }
+            reduce_rows(v, [&](int qq, int rb, float tot) {
+                const int64_t row = base + rb;
+                if (row < tile1 && q0 + qq < nq) scores[(int64_t)(q0 + qq) * n + row] = tot;
+            });
+        }
+    } else {
+        // Several queries per block: a coarse grid whose waves stream many
+        // batches each. The wave's next batch is loaded before the current
+        // one is reduced, so its loads stay in flight through the arithmetic.
+        //
+        // Loads go through one buffer descriptor for the block's rows (at
+        // most kScanMaxRows rows of at most 16 KiB): a row's byte offset is a
+        // wave-uniform scalar and each lane adds a fixed unit offset, so a
+        // load needs no address registers of its own. Every load is issued
+        // unconditionally, so the loads of a batch go out together: a row
+        // past the share re-reads the share's last row and a unit past the
+        // row re-reads the row's last unit (zeroed before use: its query
+        // unit is zero, and the bank unit need not be finite).
+        //
+        // The scores are collected in shared memory and written out at the
+        // end, row-contiguous per query: a global store inside the loop
+        // would make it wait for the prefetched loads each time (a store's
+        // registers are reused only after it completes, and loads and stores
+        // complete in one counter).
+        __shared__ float s_out[NQB][kScanMaxRows];
+        const rsrc_t brs = make_rsrc(B + tile0 * chunks, (uint32_t)((tile1 - tile0) * chunks * 16));
+        uint32_t col_off[CPL], col_mask[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            col_off[c] = (uint32_t)min(lane + c * kWave, chunks - 1) * 16u;
+            col_mask[c] = lane + c * kWave < chunks ? ~0u : 0u;
+        }
+        auto load_rows = [&](int64_t b, uint4 (&v)[RB][CPL]) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+                const uint32_t roff =
+                    (uint32_t)(min(b + rb, tile1 - 1) - tile0) * (uint32_t)chunks * 16u;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) v[rb][c] = buffer_load16_stream(brs, col_off[c], roff);
+            }
+        };
+        auto reduce_batch = [&](int64_t b, uint4 (&v)[RB][CPL]) {
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+                    v[rb][c].x &= col_mask[c];
+                    v[rb][c].y &= col_mask[c];
+                    v[rb][c].z &= col_mask[c];
+                    v[rb][c].w &= col_mask[c];
+                }
+            reduce_rows(v, [&](int qq, int rb, float tot) {
+                if (b + rb < tile1) s_out[qq][b + rb - tile0] = tot;
+            });
+        };
+        // The last batch is reduced on a path of its own, so that on every
+        // path the number of loads in flight is fixed and the wait before
+        // each reduction covers exactly its own batch.
+        if (base < tile1) {
+            uint4 v0[RB][CPL], v1[RB][CPL];
+            load_rows(base, v0);
+            for (;;) {
+                if (base + kStep >= tile1) {
+                    reduce_batch(base, v0);
+                    break;
+                }
+                load_rows(base + kStep, v1);
+                // keep the scheduler from sinking the loads below the arithmetic
+                __builtin_amdgcn_sched_barrier(0);
+                reduce_batch(base, v0);
+                base += kStep;
+                if (base + kStep >= tile1) {
+                    reduce_batch(base, v1);
+                    break;
+                }
+                load_rows(base + kStep, v0);
+                __builtin_amdgcn_sched_barrier(0);
+                reduce_batch(base, v1);
+                base += kStep;
+            }
+        }
+        __syncthreads();
+        const int rows = (int)(tile1 - tile0);
+#pragma unroll
+        for (int qq = 0; qq < NQB; ++qq) {
+            if (q0 + qq >= nq) break;
+            float* out = scores + (int64_t)(q0 + qq) * n + tile0;
+            for (int r = threadIdx.x; r < rows; r += 256) out[r] = s_out[qq][r];
         }
     }
 }
@@ -235,28 +357,6 @@ constexpr int kMmThreads = kMmRowGroups * 2 * 64;  // row groups x 2 query group
 constexpr int kMmDepth = 2;      // chunks in flight per thread
 constexpr int kMmSlots = kMmRows * 8 / kMmThreads;  // 16-byte staging slots per thread
 constexpr int kMmMaxBlocks = 1024;
-
-// Raw buffer descriptors: loads at byte offsets >= the descriptor's size
-// read zero, which pads ragged row tiles and reduction chunks for free.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family raw buffer format word
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
-                                             kRsrcWord3);
-}
-
-__device__ __forceinline__ uint4 buffer_load16(rsrc_t r, uint32_t off) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
-    return make_uint4(v[0], v[1], v[2], v[3]);
-}
-// The same with the non-temporal hint (cache-policy bit 1): bank rows are
-// streamed once per call (3% less time for the 1M-row scan than ordinary
-// loads); the queries, re-read for every row tile, keep ordinary loads.
-__device__ __forceinline__ uint4 buffer_load16_stream(rsrc_t r, uint32_t off) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);
-    return make_uint4(v[0], v[1], v[2], v[3]);
-}
 
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond any descriptor here (<= 4 MiB)
 
