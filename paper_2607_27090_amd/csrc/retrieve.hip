@@ -436,7 +436,7 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
     // swizzled unit offset per reduction step serves all of them
     const uint4* pa = &sA[0][(wr * kMmWaveRows + (lane & 31)) * 8];
     const uint4* pb = &sB[0][(wq * 128 + (lane & 31)) * 8];
-    auto compute = [&](int buf) {
+    auto compute = [&](int buf, auto&& after_ks) {
 #pragma unroll
         for (int ks = 0; ks < kMmK / 16; ++ks) {
             const int off = buf * (kMmRows * 8) + ((ks * 2 + (lane >> 5)) ^ swz(lane & 31));
@@ -451,6 +451,20 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
 #pragma unroll
                 for (int b = 0; b < 4; ++b)
                     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+            after_ks(ks);
+        }
+        // instruction order per reduction step: its fragment reads, then the
+        // two staging writes of after_ks spread among its matrix ops (left to
+        // itself the scheduler gathers all writes after the last matrix op,
+        // where nothing overlaps them)
+#pragma unroll
+        for (int ks = 0; ks < kMmK / 16; ++ks) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);  // fragment reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // matrix ops
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // staging writes
+            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // matrix ops
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // staging writes
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // matrix ops
         }
     };
 
@@ -551,9 +565,16 @@ __global__ __launch_bounds__(kMmThreads) void scan_mfma_kernel(
                 // issue the loads before this step's matrix work (the
                 // scheduler would otherwise sink them below it)
                 __builtin_amdgcn_sched_barrier(0);
-                compute(buf);
-                if (s + 1 < steps)
-                    store_chunk(buf ^ 1, ra[(p + 1) % kMmDepth], rb[(p + 1) % kMmDepth]);
+                // the next chunk is staged slot by slot between this chunk's
+                // reduction steps, so its shared-memory writes overlap the
+                // matrix work (the buffer written was last read before the
+                // previous barrier)
+                compute(buf, [&](int ks) {
+                    static_assert(kMmSlots == kMmK / 16, "one staging slot per reduction step");
+                    const int r = r_t + kRowStep * ks;
+                    sA[buf ^ 1][r * 8 + (u_t ^ swz(r))] = ra[(p + 1) % kMmDepth][ks];
+                    sB[buf ^ 1][r * 8 + (u_t ^ swz(r))] = rb[(p + 1) % kMmDepth][ks];
+                });
                 __syncthreads();
             }
         }
