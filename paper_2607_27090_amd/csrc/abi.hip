@@ -107,7 +107,7 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
         uint64_t* regions = (uint64_t*)(ws + fl.regions_off);
         e = is::launch_scan_mfma(query_emb, bank, d, nq, 0, S, sc, S, st);
         if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
-        e = is::launch_select_scores(sc, S, k, nq, 1, first, nullptr, nullptr, st);
+        e = is::launch_select_scores(sc, S, k, nq, 1, first, st);
         if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
         e = is::launch_scan_mfma_filter(query_emb, bank, d, nq, S, n, first, k, regions, counts,
                                         st);
@@ -132,8 +132,13 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
     }
     uint64_t* a = (uint64_t*)(ws + lay.cand_a_off);
     uint64_t* b = (uint64_t*)(ws + lay.cand_b_off);
-    e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, nullptr, nullptr, st);
+    e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+    if (is::merge_ranked_applies(lay.nchunks, k)) {
+        e = is::launch_merge_ranked(a, lay.nchunks, k, nq, out_ids, out_scores, st);
+        if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+        return ok();
+    }
     int64_t M = (int64_t)lay.nchunks * k;
     const int64_t chunk = is::select_chunk_len();
     while (M > chunk) {

@@ -30,9 +30,15 @@ hipError_t launch_scan_mfma_filter(const void* query, const void* bank, int d, i
                                    int64_t row_begin, int64_t row_end, const uint64_t* tau_keys,
                                    int k, uint64_t* regions, uint32_t* counts, hipStream_t st);
 int64_t select_chunk_len();
+// The k winners of each select_chunk_len() chunk of fp32 scores [nq][n], as
+// keys best first and 0-padded, to cand[q][chunk][k].
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
-                                uint64_t* cand, int32_t* out_ids, float* out_scores,
-                                hipStream_t st);
+                                uint64_t* cand, hipStream_t st);
+// Final ranking of nlists such winner lists per query (lists[q][nlists][k]),
+// for nlists * k up to the bound merge_ranked_applies checks.
+bool merge_ranked_applies(int nlists, int k);
+hipError_t launch_merge_ranked(const uint64_t* lists, int nlists, int k, int nq, int32_t* out_ids,
+                               float* out_scores, hipStream_t st);
 // Final ranking of one chunk of fp32 scores per query (n <= select_chunk_len()).
 hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, int32_t* out_ids,
                                float* out_scores, hipStream_t st);

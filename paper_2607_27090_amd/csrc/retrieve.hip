@@ -13,14 +13,16 @@
 //       operands staged through LDS, writing every score or only those not
 //       below a per-query threshold.
 //  2. select: the k largest 64-bit rank keys (score bits, ~id) per query.
-//     A 1024-thread workgroup holds up to 16384 keys in registers, bounds
-//     the answer from below (the smallest of k group maxima; for one chunk
-//     of fp32 scores, a radix bracket of the thread maxima), gathers the
-//     few keys above the bound and ranks them pairwise (a radix select
-//     takes over when many keys tie). Larger inputs go in chunks whose k
-//     winners a final pass ranks; the survivors of the filtered
-//     matrix-core scan are ranked by select_regions_kernel. Ties go to the
-//     lower id (score desc, id asc).
+//     A 1024-thread workgroup holds up to 16384 scores in registers, bounds
+//     the answer from below (a radix bracket of the thread maxima), gathers
+//     the few keys above the bound and ranks them pairwise (a radix select
+//     takes over when many keys tie). Larger inputs go in chunks of 16384
+//     whose sorted k winners are merged by rank (each key's position in its
+//     list plus binary searches in the others), or, beyond that kernel's
+//     size, ranked again in chunks of keys (the smallest of k group maxima
+//     bounds those); the survivors of the filtered matrix-core scan are
+//     ranked by select_regions_kernel. Ties go to the lower id (score desc,
+//     id asc).
 #include "wave.hpp"
 #include "launch.hpp"
 
@@ -843,14 +845,10 @@ __device__ int select_block(const uint64_t (&key)[kSelKpt], int k, SelShared& sh
     return want;
 }
 
-// Top-k of one chunk of up to kSelThreads * kSelKpt inputs per block.
-// FROM_SCORES: inputs are fp32 scores [nq][M] and a key's id is its index;
-// otherwise inputs are keys [nq][M] where 0 marks an empty entry. With
-// out_ids the block writes the final ranking, else its `k` winners (0-padded)
-// to cand_out[q][chunk][k].
-template <bool FROM_SCORES>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores,
-                                                             const uint64_t* __restrict__ keys_in,
+// Top-k of one chunk of up to kSelThreads * kSelKpt keys per block (keys
+// [nq][M], 0 marks an empty entry). With out_ids the block writes the final
+// ranking, else its `k` winners (0-padded) to cand_out[q][chunk][k].
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const uint64_t* __restrict__ keys_in,
                                                              int64_t M, int k, int nchunks,
                                                              uint64_t* __restrict__ cand_out,
                                                              int32_t* __restrict__ out_ids,
@@ -860,29 +858,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     const int q = blockIdx.y;
     const int64_t c0 = (int64_t)blockIdx.x * (kSelThreads * kSelKpt);
 
+    // every load is issued before the first is used: an index past the end
+    // re-reads the last key (M >= 1), which is then dropped
     uint64_t key[kSelKpt];
-    if (FROM_SCORES) {
-        // every load is issued before the first is used: an index past the
-        // end re-reads the last score (M >= 1), whose value is then dropped
-        // (a load under a per-element condition is compiled into its own
-        // branch, and each branch waits for its load)
-        float v[kSelKpt];
 #pragma unroll
-        for (int i = 0; i < kSelKpt; ++i) {
-            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
-            v[i] = scores[(int64_t)q * M + (idx < M ? idx : M - 1)];
-        }
+    for (int i = 0; i < kSelKpt; ++i) {
+        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
+        key[i] = keys_in[(int64_t)q * M + (idx < M ? idx : M - 1)];
+    }
 #pragma unroll
-        for (int i = 0; i < kSelKpt; ++i) {
-            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;
-            key[i] = idx < M ? rank_key(v[i], (uint32_t)idx) : 0ull;
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < kSelKpt; ++i) {
-            const int64_t idx = c0 + t + (int64_t)i * kSelThreads;  // coalesced
-            key[i] = idx < M ? keys_in[(int64_t)q * M + idx] : 0ull;
-        }
+    for (int i = 0; i < kSelKpt; ++i) {
+        const int64_t idx = c0 + t + (int64_t)i * kSelThreads;
+        key[i] = idx < M ? key[i] : 0ull;
     }
     // key[i] is nonzero iff valid: ~id has its top bit set for ids < 2^31
     const int want = select_block(key, k, sh);
@@ -935,16 +922,24 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 //    are gathered in LDS (each wave reserves its run with one atomic) and
 //    ranked pairwise. Should there be more than kSelRankMax of them (many
 //    tied scores), the general select over 64-bit keys takes over.
+//
+// With cand_out the block ranks chunk blockIdx.x (kSelThreads * KPT scores
+// from index blockIdx.x * kSelThreads * KPT of the query's row of Mrow) and
+// writes its k winners as keys, best first and 0-padded, to
+// cand_out[q][chunk][k]; otherwise the row (M = Mrow scores) is one chunk
+// and the ranking goes to out_ids / out_scores.
 template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
-    const float* __restrict__ scores, int64_t M, int k, int32_t* __restrict__ out_ids,
-    float* __restrict__ out_scores) {
+    const float* __restrict__ scores, int64_t Mrow, int k, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_scores, uint64_t* __restrict__ cand_out, int nchunks) {
     __shared__ SelShared sh;
     __shared__ uint32_t s_hist2[256];   // radix passes alternate between sh.hist and this
     __shared__ uint32_t s_ncand;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int q = blockIdx.y;
-    const float* sq = scores + (int64_t)q * M;
+    const int64_t base = cand_out ? (int64_t)blockIdx.x * (kSelThreads * KPT) : 0;
+    const int64_t M = cand_out ? min_i64(Mrow - base, (int64_t)kSelThreads * KPT) : Mrow;
+    const float* sq = scores + (int64_t)q * Mrow + base;
     // all loads issued before the first is used (an index past the end
     // re-reads the last score, M >= 1, and is then dropped)
     float sv[KPT];
@@ -1075,7 +1070,7 @@ __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
         for (int i = 0; i < KPT; ++i) {
             if (mask[i]) {  // wave-uniform: most of the masks are empty
                 if (u[i] >= tau && i < nv) {
-                    const uint32_t idx = (uint32_t)(t + i * kSelThreads);
+                    const uint32_t idx = (uint32_t)(base + t + i * kSelThreads);
                     const uint32_t slot = at + lanes_below(mask[i]);
                     if (slot < (uint32_t)kSelRankMax)
                         sh.cand[slot] = ((uint64_t)u[i] << 32) | (uint64_t)(~idx);
@@ -1093,17 +1088,61 @@ __global__ __launch_bounds__(kSelThreads) void select_small_kernel(
         uint64_t key[kSelKpt];
 #pragma unroll
         for (int i = 0; i < kSelKpt; ++i) {
-            const uint32_t idx = (uint32_t)(t + i * kSelThreads);
+            const uint32_t idx = (uint32_t)(base + t + i * kSelThreads);
             key[i] = (i < KPT && i < nv) ? (((uint64_t)u[i] << 32) | (uint64_t)(~idx)) : 0ull;
         }
         got = select_block(key, k, sh);
     }
 
     // ---- output, best first ----
+    if (cand_out) {
+        uint64_t* dst = cand_out + ((int64_t)q * nchunks + blockIdx.x) * k;
+        for (int i = t; i < k; i += kSelThreads) dst[i] = i < got ? sh.sel[i] : 0ull;
+        return;
+    }
     for (int i = t; i < got; i += kSelThreads) {
         const uint64_t me = sh.sel[i];
         out_ids[(int64_t)q * k + i] = (int32_t)key_id(me);
         if (out_scores) out_scores[(int64_t)q * k + i] = key_score(me);
+    }
+}
+
+// Final ranking of per-chunk winner lists: nlists lists of k keys per query,
+// each best first and 0-padded, all keys distinct. A key's rank is its
+// position in its own list plus, in every other list, the number of keys
+// above it (a binary search), so one pass over the lists in shared memory
+// ranks them all; the keys ranked below k are the answer.
+constexpr int kMergeMax = 4096;  // keys per query at most
+
+__global__ __launch_bounds__(kSelThreads) void merge_ranked_kernel(
+    const uint64_t* __restrict__ lists, int nlists, int k, int32_t* __restrict__ out_ids,
+    float* __restrict__ out_scores) {
+    __shared__ uint64_t s[kMergeMax];
+    const int q = blockIdx.x;
+    const int total = nlists * k;
+    const uint64_t* src = lists + (int64_t)q * total;
+    for (int e = threadIdx.x; e < total; e += kSelThreads) s[e] = src[e];
+    __syncthreads();
+    for (int e = threadIdx.x; e < total; e += kSelThreads) {
+        const uint64_t x = s[e];
+        if (x == 0) continue;  // padding
+        const int c = e / k;
+        int rank = e - c * k;
+        for (int c2 = 0; c2 < nlists; ++c2) {
+            if (c2 == c) continue;
+            const uint64_t* l = s + c2 * k;
+            int lo = 0, hi = k;  // first position whose key is below x
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (l[mid] > x) lo = mid + 1;
+                else hi = mid;
+            }
+            rank += lo;
+        }
+        if (rank < k) {
+            out_ids[(int64_t)q * k + rank] = (int32_t)key_id(x);
+            if (out_scores) out_scores[(int64_t)q * k + rank] = key_score(x);
+        }
     }
 }
 
@@ -1192,11 +1231,20 @@ __global__ __launch_bounds__(kSelThreads) void select_regions_kernel(
 int64_t select_chunk_len() { return (int64_t)kSelThreads * kSelKpt; }
 
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
-                                uint64_t* cand, int32_t* out_ids, float* out_scores,
-                                hipStream_t st) {
+                                uint64_t* cand, hipStream_t st) {
     dim3 grid((unsigned)nchunks, (unsigned)nq);
-    hipLaunchKernelGGL((select_kernel<true>), grid, dim3(kSelThreads), 0, st, scores,
-                       (const uint64_t*)nullptr, n, k, nchunks, cand, out_ids, out_scores);
+    hipLaunchKernelGGL((select_small_kernel<kSelKpt>), grid, dim3(kSelThreads), 0, st, scores, n,
+                       k, (int32_t*)nullptr, (float*)nullptr, cand, nchunks);
+    return hipGetLastError();
+}
+
+bool merge_ranked_applies(int nlists, int k) { return (int64_t)nlists * k <= kMergeMax; }
+
+hipError_t launch_merge_ranked(const uint64_t* lists, int nlists, int k, int nq, int32_t* out_ids,
+                               float* out_scores, hipStream_t st) {
+    if (!merge_ranked_applies(nlists, k)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(merge_ranked_kernel, dim3((unsigned)nq), dim3(kSelThreads), 0, st, lists,
+                       nlists, k, out_ids, out_scores);
     return hipGetLastError();
 }
 
@@ -1206,7 +1254,7 @@ hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, in
     dim3 grid(1u, (unsigned)nq);
 #define IS_SELECT_SMALL(KPT)                                                                      \
     hipLaunchKernelGGL((select_small_kernel<KPT>), grid, dim3(kSelThreads), 0, st, scores, n, k,  \
-                       out_ids, out_scores)
+                       out_ids, out_scores, (uint64_t*)nullptr, 1)
     if (kpt <= 4) IS_SELECT_SMALL(4);
     else if (kpt <= 8) IS_SELECT_SMALL(8);
     else if (kpt <= 12) IS_SELECT_SMALL(12);
@@ -1219,8 +1267,8 @@ hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, in
 hipError_t launch_select_keys(const uint64_t* keys, int64_t M, int k, int nq, int nchunks,
                               uint64_t* cand, int32_t* out_ids, float* out_scores, hipStream_t st) {
     dim3 grid((unsigned)nchunks, (unsigned)nq);
-    hipLaunchKernelGGL((select_kernel<false>), grid, dim3(kSelThreads), 0, st,
-                       (const float*)nullptr, keys, M, k, nchunks, cand, out_ids, out_scores);
+    hipLaunchKernelGGL(select_kernel, grid, dim3(kSelThreads), 0, st, keys, M, k, nchunks, cand,
+                       out_ids, out_scores);
     return hipGetLastError();
 }
 
