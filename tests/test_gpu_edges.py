@@ -31,6 +31,9 @@ def _ret_case(n, d, k, nq, dt, shared, seed):
     (16385, 32, 7, 1, "f32", True),          # one key into a second chunk
     (20000, 32, 1024, 2, "f32", True),       # largest k, two chunks
     (300000, 16, 1024, 1, "f32", True),      # multi-level candidate merge
+    (65536, 16, 1024, 1, "f32", True),       # 4 x 1024 chunk winners: merged by rank
+    (65537, 16, 1024, 1, "f32", True),       # 5 x 1024: one list past the rank merge
+    (100000, 16, 100, 8, "bf16", True),      # 8 queries per row load, rows of 2 units
     (5000, 1024, 100, 3, "bf16", True),      # several queries share each row load
     (2000, 768, 50, 5, "f32", False),        # one bank per query
     (777, 264, 7, 9, "bf16", True),          # ragged d, 9 queries over 2 groups
