@@ -92,8 +92,6 @@ __device__ __forceinline__ uint4 load_stream(const uint4* p) {
     return make_uint4(x.x, x.y, x.z, x.w);
 }
 
-// One block = 4 waves. blockIdx.y selects a group of NQB queries (shared
-// bank) or one query and its own bank (per-query banks, NQB == 1).
 // Raw buffer descriptors: loads at byte offsets >= the descriptor's size
 // read zero, which pads ragged row tiles and reduction chunks for free.
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -118,6 +116,8 @@ __device__ __forceinline__ uint4 buffer_load16_stream(rsrc_t r, uint32_t off, ui
 
 constexpr int kScanMaxRows = 1024;  // rows per block at most
 
+// One block = 4 waves. blockIdx.y selects a group of NQB queries (shared
+// bank) or one query and its own bank (per-query banks, NQB == 1).
 template <class Tag, int CPL, int NQB, int RB>
 __global__ __launch_bounds__(256) void scan_kernel(const uint4* __restrict__ query,
                                                    const uint4* __restrict__ bank, int64_t n,
