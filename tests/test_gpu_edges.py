@@ -179,6 +179,24 @@ def test_retrieve_filtered_scan_negative_scores():
     log(f"filtered scan, negative scores: near-tie swaps {near}")
 
 
+def test_retrieve_ties_across_select_chunks():
+    # 30 rows at the start of each of four 16,384-score select chunks share
+    # the top score, every other row scores 0: the chunks' winner lists are
+    # merged by rank, and the tied keys order by id across the lists
+    n, d, k = 4 * 16384, 8, 100
+    bank = torch.zeros(n, d, device="cuda")
+    top = [c * 16384 + j for c in range(4) for j in range(30)]
+    bank[top, 0] = 1.0
+    q = torch.zeros(2, d, device="cuda")
+    q[:, 0] = 1.0
+    buf = RequestBuffers(n=n, d=d, k=k, nq=2, emb_dtype=torch.float32, max_tokens=1)
+    buf.retrieve(q, bank)
+    torch.cuda.synchronize()
+    for r in range(2):
+        assert buf.ids[r].tolist() == top[:k]
+        assert (buf.scores[r] == 1.0).all()
+
+
 def test_retrieve_signed_zero_scores_tie():
     # every score is +0 or -0: they are equal, so ranks follow the ids
     n, d = 500, 16
