@@ -60,7 +60,7 @@ extern "C" {
 /* return codes */
 #define IS_OK 0
 #define IS_ERR_INVALID (-1)      /* bad argument detected on the host        */
-#define IS_ERR_UNSUPPORTED (-2)  /* valid but not supported by this build    */
+#define IS_ERR_UNSUPPORTED (-2)  /* valid but not supported by the library  */
 #define IS_ERR_WORKSPACE (-3)    /* workspace missing or too small           */
 #define IS_ERR_HIP (-4)          /* the HIP runtime refused a launch         */
 
@@ -77,7 +77,7 @@ extern "C" {
 #define IS_DEV_SLOT_RANGE 32u /* a slot outside [0, num_slots)                      */
 #define IS_DEV_SRC_RANGE 64u  /* a fact's stored rows fall outside [0, T_store)      */
 
-/* limits of this build */
+/* limits of the library */
 #define IS_MAX_K 1024         /* largest k                                           */
 #define IS_MAX_HEAD_DIM 512   /* largest head dimension D                            */
 
