@@ -55,22 +55,37 @@ RetrieveLayout retrieve_layout(int64_t n, int32_t k, int32_t nq) {
 }
 
 // Filtered matrix-core retrieval (many queries on one shared bf16 bank): the
-// scores of a sample of the first S rows [nq][S], the sample's winners
-// [nq][k], survivor counts [nq][G] and survivor regions [nq][G][rows per
-// block], where G * rows per block <= (n - S) + 32 G (G <= the block bound).
+// scores of a sample of the first S rows [nq][S], the winners of each of its
+// select chunks [nq][S / chunk][k] (several chunks only), the sample's
+// winners [nq][k], survivor counts [nq][G] and survivor regions [nq][G][rows
+// per block], where G * rows per block <= (n - S) + 32 G (G <= the block
+// bound).
 struct FusedLayout {
-    size_t scores_off, first_off, counts_off, regions_off, total;
+    size_t scores_off, chunks_off, first_off, counts_off, regions_off, total;
     int64_t sample;
 };
 
+// The sample: one to four select chunks, at most a quarter of the bank. Its
+// dense scan takes one row tile per block whatever its size up to a row tile
+// per CU, and a larger sample leaves fewer rows to the filtered scan and a
+// tighter bound (the 1M-row bank: 65,536 rows).
+int64_t fused_sample(int64_t n) {
+    const int64_t chunk = is::select_chunk_len();
+    const int64_t c = std::min<int64_t>(4, std::max<int64_t>(1, n / (4 * chunk)));
+    return c * chunk;
+}
+
 FusedLayout fused_layout(int64_t n, int32_t k, int32_t nq) {
     FusedLayout lay{};
-    const int64_t S = is::select_chunk_len();
+    const int64_t S = fused_sample(n);
+    const int64_t nch = S / is::select_chunk_len();
     const int64_t gmax = is::mfma_max_blocks();
     lay.sample = S;
     size_t off = 0;
     lay.scores_off = off;
     off = round_up(off + (size_t)nq * S * sizeof(float), 256);
+    lay.chunks_off = off;
+    if (nch > 1) off = round_up(off + (size_t)nq * nch * k * sizeof(uint64_t), 256);
     lay.first_off = off;
     off = round_up(off + (size_t)nq * k * sizeof(uint64_t), 256);
     lay.counts_off = off;
@@ -107,7 +122,15 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
         uint64_t* regions = (uint64_t*)(ws + fl.regions_off);
         e = is::launch_scan_mfma(query_emb, bank, d, nq, 0, S, sc, S, st);
         if (e != hipSuccess) return fail(IS_ERR_HIP, "scan launch: %s", hipGetErrorString(e));
-        e = is::launch_select_scores(sc, S, k, nq, 1, first, st);
+        const int nch = (int)(S / is::select_chunk_len());
+        if (nch == 1) {
+            e = is::launch_select_scores(sc, S, k, nq, 1, first, st);
+        } else {
+            uint64_t* chunks = (uint64_t*)(ws + fl.chunks_off);
+            e = is::launch_select_scores(sc, S, k, nq, nch, chunks, st);
+            if (e == hipSuccess)
+                e = is::launch_merge_ranked(chunks, nch, k, nq, nullptr, nullptr, first, st);
+        }
         if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
         e = is::launch_scan_mfma_filter(query_emb, bank, d, nq, S, n, first, k, regions, counts,
                                         st);
@@ -135,7 +158,7 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
     e = is::launch_select_scores(scores, n, k, nq, lay.nchunks, a, st);
     if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
     if (is::merge_ranked_applies(lay.nchunks, k)) {
-        e = is::launch_merge_ranked(a, lay.nchunks, k, nq, out_ids, out_scores, st);
+        e = is::launch_merge_ranked(a, lay.nchunks, k, nq, out_ids, out_scores, nullptr, st);
         if (e != hipSuccess) return fail(IS_ERR_HIP, "select launch: %s", hipGetErrorString(e));
         return ok();
     }

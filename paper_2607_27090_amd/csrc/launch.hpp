@@ -35,10 +35,12 @@ int64_t select_chunk_len();
 hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, int nchunks,
                                 uint64_t* cand, hipStream_t st);
 // Final ranking of nlists such winner lists per query (lists[q][nlists][k]),
-// for nlists * k up to the bound merge_ranked_applies checks.
+// for nlists * k up to the bound merge_ranked_applies checks: to out_ids /
+// out_scores, or with out_keys as keys best first (0-padded) to
+// out_keys[q][k].
 bool merge_ranked_applies(int nlists, int k);
 hipError_t launch_merge_ranked(const uint64_t* lists, int nlists, int k, int nq, int32_t* out_ids,
-                               float* out_scores, hipStream_t st);
+                               float* out_scores, uint64_t* out_keys, hipStream_t st);
 // Final ranking of one chunk of fp32 scores per query (n <= select_chunk_len()).
 hipError_t launch_select_small(const float* scores, int64_t n, int k, int nq, int32_t* out_ids,
                                float* out_scores, hipStream_t st);

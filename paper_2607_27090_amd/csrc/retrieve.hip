@@ -1116,12 +1116,16 @@ constexpr int kMergeMax = 4096;  // keys per query at most
 
 __global__ __launch_bounds__(kSelThreads) void merge_ranked_kernel(
     const uint64_t* __restrict__ lists, int nlists, int k, int32_t* __restrict__ out_ids,
-    float* __restrict__ out_scores) {
+    float* __restrict__ out_scores, uint64_t* __restrict__ out_keys) {
     __shared__ uint64_t s[kMergeMax];
     const int q = blockIdx.x;
     const int total = nlists * k;
     const uint64_t* src = lists + (int64_t)q * total;
     for (int e = threadIdx.x; e < total; e += kSelThreads) s[e] = src[e];
+    // key output: every position starts empty (the barrier orders these
+    // writes before the ranked ones)
+    if (out_keys)
+        for (int i = threadIdx.x; i < k; i += kSelThreads) out_keys[(int64_t)q * k + i] = 0ull;
     __syncthreads();
     for (int e = threadIdx.x; e < total; e += kSelThreads) {
         const uint64_t x = s[e];
@@ -1140,8 +1144,12 @@ __global__ __launch_bounds__(kSelThreads) void merge_ranked_kernel(
             rank += lo;
         }
         if (rank < k) {
-            out_ids[(int64_t)q * k + rank] = (int32_t)key_id(x);
-            if (out_scores) out_scores[(int64_t)q * k + rank] = key_score(x);
+            if (out_keys) {
+                out_keys[(int64_t)q * k + rank] = x;
+            } else {
+                out_ids[(int64_t)q * k + rank] = (int32_t)key_id(x);
+                if (out_scores) out_scores[(int64_t)q * k + rank] = key_score(x);
+            }
         }
     }
 }
@@ -1241,10 +1249,10 @@ hipError_t launch_select_scores(const float* scores, int64_t n, int k, int nq, i
 bool merge_ranked_applies(int nlists, int k) { return (int64_t)nlists * k <= kMergeMax; }
 
 hipError_t launch_merge_ranked(const uint64_t* lists, int nlists, int k, int nq, int32_t* out_ids,
-                               float* out_scores, hipStream_t st) {
+                               float* out_scores, uint64_t* out_keys, hipStream_t st) {
     if (!merge_ranked_applies(nlists, k)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(merge_ranked_kernel, dim3((unsigned)nq), dim3(kSelThreads), 0, st, lists,
-                       nlists, k, out_ids, out_scores);
+                       nlists, k, out_ids, out_scores, out_keys);
     return hipGetLastError();
 }
 

@@ -165,6 +165,25 @@ def test_retrieve_filtered_scan_every_row_survives():
     log(f"filtered scan, all rows survive for one query: near-tie swaps {near}")
 
 
+def test_retrieve_filtered_scan_four_chunk_sample():
+    # a bank of 300,000 rows takes a sample of four select chunks (65,536
+    # rows), whose chunk winners are merged by rank into the bound; the
+    # rows after the sample all equal query 0, so for it every one of them
+    # survives the filter, and its ties go to the lower ids
+    g = torch.Generator(device="cuda").manual_seed(93)
+    n, d, k, nq, S = 300_000, 64, 50, 32, 4 * 16384
+    bank = torch.randn(n, d, generator=g, device="cuda")
+    bank = (bank / bank.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    v = bank[7].clone()
+    bank[S:] = v
+    q = (torch.randn(nq, d, generator=g, device="cuda"))
+    q = (q / q.norm(dim=1, keepdim=True)).to(torch.bfloat16)
+    q[0] = v
+    gids, near = _ranked_against_oracle(q, bank, k)
+    assert gids[0][0] == 7 and list(gids[0][1:]) == list(range(S, S + k - 1))
+    log(f"filtered scan, four-chunk sample, all rows survive for one query: near-tie swaps {near}")
+
+
 def test_retrieve_filtered_scan_negative_scores():
     # every score is negative, so the sample threshold is below the zero
     # scores of the padding rows of partial tiles: they must not be ranked
