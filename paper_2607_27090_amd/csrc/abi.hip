@@ -111,9 +111,10 @@ int enqueue_retrieve(const void* query_emb, const void* bank, int64_t n, int32_t
     char* ws = (char*)workspace;
     hipError_t e;
     if (fused) {
-        // 1. dense scores of the first S rows; 2. their k winners, whose k-th
-        // key bounds the answer from below; 3. the rest of the bank keeps
-        // only keys above it; 4. exact ranking of sample winners + survivors
+        // 1. dense scores of the first S rows; 2. their k winners (per select
+        // chunk, then merged by rank), whose k-th key bounds the answer from
+        // below; 3. the rest of the bank keeps only keys above it; 4. exact
+        // ranking of sample winners + survivors
         const FusedLayout fl = fused_layout(n, k, nq);
         const int64_t S = fl.sample;
         float* sc = (float*)(ws + fl.scores_off);
