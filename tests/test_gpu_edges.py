@@ -34,6 +34,7 @@ def _ret_case(n, d, k, nq, dt, shared, seed):
     (65536, 16, 1024, 1, "f32", True),       # 4 x 1024 chunk winners: merged by rank
     (65537, 16, 1024, 1, "f32", True),       # 5 x 1024: one list past the rank merge
     (100000, 16, 100, 8, "bf16", True),      # 8 queries per row load, rows of 2 units
+    (30000, 1000, 20, 5, "f32", True),       # 4 queries per row load, ragged row, 4 + 1
     (5000, 1024, 100, 3, "bf16", True),      # several queries share each row load
     (2000, 768, 50, 5, "f32", False),        # one bank per query
     (777, 264, 7, 9, "bf16", True),          # ragged d, 9 queries over 2 groups
