@@ -396,6 +396,50 @@ def main():
     inj_launch_ms = ei0.elapsed_time(ei1) / (args.steps * nwaves)
     log(f"inject alone: {inj_launch_ms * 1e3:.1f} us per launch")
 
+    # ---- the same launches with each request's blocks in a small pool ----------
+    # (a side figure for how the pages' spread over the pool sets the inject's
+    # rate: the timed steps draw each request's blocks at random from one of R
+    # regions of a pool of 1.1 x R x max_blocks blocks; here they come from a
+    # pool of 1.1 x max_blocks, as in the tests)
+    dense_pool = None
+    if fused and w.nq == 1 and not host_store and args.rope == "default":
+        dbt, dnb = workloads.make_block_tables(w, dev, variant=1)
+        dpk, dpv, dns = workloads.make_pages(w, dnb, dev)
+        # own placement outputs: the timed steps' ones stay for the parity check
+        d_slots = torch.empty(1, w.max_tokens, dtype=torch.int64, device=dev)
+        d_pos = torch.empty(1, w.max_tokens, dtype=torch.int32, device=dev)
+        d_m = torch.empty(len(sets), dtype=torch.int32, device=dev)
+        d_status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+        def dense_launch(si):
+            is_place_inject(sets[si].ids, store["preK"], store["V"], w.theta, dpk, dpv, d_slots,
+                            d_pos, d_m[si:si + 1], fact_offsets=offs, fact_lens=lens,
+                            start_pos=w.start_pos, block_table=dbt, page_size=w.page_size,
+                            max_blocks=dbt.shape[-1], k=w.k, nq=1, n=w.n, lens_stride=lens_stride,
+                            max_tokens=w.max_tokens, L=L, H=H, D=D, T_store=T, num_slots=dns,
+                            status=d_status)
+        for si in range(min(2, len(sets))):
+            dense_launch(si)
+        ed0, ed1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ed0.record()
+        for si in range(len(sets)):
+            dense_launch(si)
+        ed1.record()
+        torch.cuda.synchronize()
+        assert int(d_status.item()) == 0, "device status flags raised"
+        d_ms = ed0.elapsed_time(ed1) / args.steps
+        dm = d_m.cpu().tolist()
+        d_bytes = statistics.fmean(
+            workloads.inject_algorithmic_bytes(w, m) + 12 * m for m in dm)
+        d_gbps = d_bytes / (d_ms * 1e-3) / 1e9
+        dense_pool = {"pool_GB": round(2 * dpk.numel() * 2 / 1e9, 2),
+                      "timed_steps_pool_GB": round(2 * pk.numel() * 2 / 1e9, 2),
+                      "inject_launch_us": round(d_ms * 1e3, 2), "GBps": round(d_gbps, 1),
+                      "frac_of_peak": round(d_gbps / HBM_PEAK_GBPS, 4)}
+        del dpk, dpv, d_slots, d_pos
+        log(f"inject with the blocks in a {dense_pool['pool_GB']} GB pool: "
+            f"{dense_pool['inject_launch_us']} us per launch, {dense_pool['frac_of_peak']} of peak")
+
     # ---- ANN: the search alone, the exact retrieval alone, recall ------------
     if ann is not None:
         ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -679,6 +723,7 @@ def main():
         "throughput_2_streams_us_per_request": (None if two_ms is None
                                                 else round(two_ms * 1e3 / w.nq, 3)),
         "inject_launch_us": round(inj_launch_ms * 1e3, 2),
+        "inject_small_pool": dense_pool,
         "per_call_us": ({k: round(statistics.fmean(v) * 1e3, 2) for k, v in per.items()}
                         if args.detail else None),
         "latency_us_per_step": None if latency_ms is None else round(latency_ms * 1e3, 3),
